@@ -1,0 +1,171 @@
+"""CPU oracle for softmax attention and Rowmax-H15 attention (test infrastructure).
+
+TEST INFRASTRUCTURE, NOT PRODUCT CODE.  Only the test suite, the smoke check
+and the CPU-baseline leg of the benchmark may import this package.  It shares
+no code with the GPU library; the arithmetic lives in ``attn_oracle.c`` (plain
+C, fp64 accumulation), this module only marshals numpy arrays through ctypes.
+
+Paper: "Approximating Softmax in Pretrained LLMs: Model Sensitivity and Kernel
+Acceleration".  Modes follow App. A.1 Eq. (exact-attention) (EXACT),
+Sec. 5.2 Eq. (m-h15) with App. B.1 "Implementation" and the per-tile running
+max of App. B.2 (H15_TILE), the whole-row control of Table B2 (H15_WHOLEROW)
+and App. A.6 Eq. (rowmax-pot) (ROWMAX_POT).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from pathlib import Path
+
+import numpy as np
+
+from .build import build as _build, LIB_PATH
+
+BF16, FP8_E4M3 = 0, 1
+EXACT, H15_TILE, H15_WHOLEROW, ROWMAX_POT, EXACT_TILE = 0, 1, 2, 3, 4
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load the oracle library, building it first when it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not LIB_PATH.exists():
+        _build()
+    L = ctypes.CDLL(str(LIB_PATH))
+    c_f, c_d, c_i, c_i64, c_p = ctypes.c_float, ctypes.c_double, ctypes.c_int, ctypes.c_int64, ctypes.c_void_p
+    L.oracle_threads.restype = c_i
+    L.oracle_bf16_value.argtypes = [ctypes.c_uint16]
+    L.oracle_bf16_value.restype = c_d
+    L.oracle_e4m3_value.argtypes = [ctypes.c_uint8]
+    L.oracle_e4m3_value.restype = c_d
+    L.oracle_e4m3_rne_satfinite.argtypes = [c_d]
+    L.oracle_e4m3_rne_satfinite.restype = ctypes.c_uint8
+    L.oracle_h15_weight.argtypes = [c_f]
+    L.oracle_h15_weight.restype = c_f
+    L.oracle_h15_ideal.argtypes = [c_d]
+    L.oracle_h15_ideal.restype = c_d
+    L.oracle_h15_exhaustive.argtypes = [c_f, c_f, ctypes.POINTER(c_i64)]
+    L.oracle_h15_exhaustive.restype = c_i64
+    L.oracle_c1.argtypes = [c_d, c_d, c_d]
+    L.oracle_c1.restype = c_f
+    L.oracle_h15_row_from_logits.argtypes = [c_p, c_i, c_i, c_i, c_f, c_i, c_i, c_d, c_i, c_p, c_p, c_p]
+    L.oracle_h15_row_from_logits.restype = c_i
+    L.oracle_attn.argtypes = [c_p, c_p, c_p, c_i, c_d, c_d, c_d, c_i, c_i, c_i, c_i, c_i, c_i, c_d,
+                              c_i, c_i, c_d, c_p, c_i64, c_p, c_p]
+    L.oracle_attn.restype = c_i
+    L.oracle_logits_row.argtypes = [c_p, c_p, c_i, c_i, c_i, c_i, c_i, c_i, c_i, c_i, c_i, c_p]
+    L.oracle_logits_row.restype = c_i
+    _lib = L
+    return L
+
+
+def _ptr(a: np.ndarray | None):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def threads() -> int:
+    return lib().oracle_threads()
+
+
+def bf16_value(bits: int) -> float:
+    return lib().oracle_bf16_value(int(bits))
+
+
+def e4m3_value(code: int) -> float:
+    return lib().oracle_e4m3_value(int(code))
+
+
+def e4m3_encode(x: float) -> int:
+    return int(lib().oracle_e4m3_rne_satfinite(float(x)))
+
+
+def h15_weight(y: float) -> float:
+    """App. B.1 FP32 add/shift realisation on the doubled exponent y = 2x."""
+    return lib().oracle_h15_weight(float(y))
+
+
+def h15_ideal(y: float) -> float:
+    """Eq. (m-h15) closed form on the doubled exponent y = 2x (no clamp)."""
+    return lib().oracle_h15_ideal(float(y))
+
+
+def h15_exhaustive(lo: float, hi: float) -> tuple[int, int]:
+    """Compare the two forms over every fp32 value in [lo, hi]; (mismatches, count)."""
+    n = ctypes.c_int64(0)
+    bad = lib().oracle_h15_exhaustive(float(lo), float(hi), ctypes.byref(n))
+    return int(bad), int(n.value)
+
+
+def c1(scale: float, qd: float = 1.0, kd: float = 1.0) -> float:
+    """Base-two exponent scale of a raw logit, fp32(scale*qd*kd*log2 e)."""
+    return lib().oracle_c1(float(scale), float(qd), float(kd))
+
+
+def h15_row_from_logits(s: np.ndarray, i: int, causal: bool, c1_: float, dtype: int,
+                        Bc: int, tau: float = 0.0, exact_exp: bool = False):
+    """W (fp32) and P bits (bf16 or e4m3 code) of query row i from its fp32 logits.
+
+    Returns (W, P, lse)."""
+    s = np.ascontiguousarray(s, dtype=np.float32)
+    S = s.shape[0]
+    w = np.zeros(S, np.float32)
+    p = np.zeros(S, np.uint32)
+    lse = ctypes.c_double(0.0)
+    rc = lib().oracle_h15_row_from_logits(_ptr(s), S, int(i), int(bool(causal)), float(c1_), int(dtype),
+                                          int(Bc), float(tau), int(bool(exact_exp)), _ptr(w), _ptr(p),
+                                          ctypes.byref(lse))
+    if rc != 0:
+        raise ValueError("oracle_h15_row_from_logits: invalid arguments")
+    return w, p, lse.value
+
+
+def attn(q: np.ndarray, k: np.ndarray, v: np.ndarray, *, dtype: int, causal: bool, scale: float,
+         mode: int, descale=(1.0, 1.0, 1.0), Bc: int = 128, tau: float = 0.0,
+         rows: np.ndarray | None = None):
+    """Attention forward on stored operands.
+
+    q: [B,Hq,S,d], k/v: [B,Hkv,S,d]; uint16 bf16 bit patterns (dtype BF16) or
+    uint8 e4m3 codes (dtype FP8_E4M3).  rows: optional flat row indices
+    (b*Hq + h)*S + i.  Returns (O [nrows, d] float64, LSE [nrows] float64);
+    without rows the shapes are [B,Hq,S,d] and [B,Hq,S]."""
+    want = np.uint16 if dtype == BF16 else np.uint8
+    q = np.ascontiguousarray(q, dtype=want)
+    k = np.ascontiguousarray(k, dtype=want)
+    v = np.ascontiguousarray(v, dtype=want)
+    B, Hq, S, d = q.shape
+    Hkv = k.shape[1]
+    if k.shape != (B, Hkv, S, d) or v.shape != k.shape:
+        raise ValueError("shape mismatch")
+    if rows is None:
+        nrows = B * Hq * S
+        rows_arr = None
+    else:
+        rows_arr = np.ascontiguousarray(rows, dtype=np.int64)
+        nrows = rows_arr.shape[0]
+    o = np.zeros((nrows, d), np.float64)
+    lse = np.zeros(nrows, np.float64)
+    qd, kd, vd = (float(x) for x in descale)
+    rc = lib().oracle_attn(_ptr(q), _ptr(k), _ptr(v), int(dtype), qd, kd, vd, B, Hq, Hkv, S, d,
+                           int(bool(causal)), float(scale), int(mode), int(Bc), float(tau),
+                           _ptr(rows_arr), int(nrows), _ptr(o), _ptr(lse))
+    if rc != 0:
+        raise ValueError("oracle_attn: invalid arguments")
+    if rows is None:
+        return o.reshape(B, Hq, S, d), lse.reshape(B, Hq, S)
+    return o, lse
+
+
+def logits_row(q: np.ndarray, k: np.ndarray, dtype: int, b: int, h: int, i: int) -> np.ndarray:
+    """fp32 raw logits of one query row (exact fp64 dot, rounded once)."""
+    want = np.uint16 if dtype == BF16 else np.uint8
+    q = np.ascontiguousarray(q, dtype=want)
+    k = np.ascontiguousarray(k, dtype=want)
+    B, Hq, S, d = q.shape
+    out = np.zeros(S, np.float32)
+    rc = lib().oracle_logits_row(_ptr(q), _ptr(k), int(dtype), B, Hq, k.shape[1], S, d, b, h, i, _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle_logits_row: invalid arguments")
+    return out

@@ -1,0 +1,357 @@
+/*
+ * CPU oracle for softmax attention and Rowmax-H15 attention.
+ *
+ * TEST INFRASTRUCTURE, NOT PRODUCT CODE.  Only the test suite, the smoke check
+ * and the CPU-baseline leg of the benchmark may load this library.  It shares
+ * no code, header, table or constant with the GPU library: everything below is
+ * written directly from the paper's definitions.
+ *
+ * Paper: "Approximating Softmax in Pretrained LLMs: Model Sensitivity and
+ * Kernel Acceleration".  Sections cited:
+ *   App. A.1, Eq. (exact-attention)        softmax over the valid key set
+ *   Sec. 5.2 Eq. (m-h15) = App. B.1 Eq. (h15)  the Rowmax-H15 weight
+ *   App. B.1 "Implementation"              the FP32 add/shift realisation,
+ *                                          clamp, doubled exponent constants,
+ *                                          row sum and PV on the same weights
+ *   App. B.1 "Relation to classical bit-level exponentiation"
+ *                                          H = S o Q_1/2, octave-error envelope
+ *   App. B.2 "Semantic simulation"         per-tile running max (tile 128),
+ *                                          rescale threshold 0 (FP8 path)
+ *   App. B.2, Table B2                     offline whole-row control
+ *   App. A.6 Eq. (rowmax-pot)              Rowmax-PoT, K_max = 20
+ *
+ * Precision policy: everything the paper leaves to "exact" arithmetic is done
+ * in fp64 from the exactly decoded stored operands (bf16 values, or e4m3 codes
+ * read as reals).  The steps that the paper fixes in FP32 (the exponent
+ * argument, the add of 0x4B400000, the shift) are done in FP32 exactly as
+ * stated.  Build with -ffp-contract=off and without -ffast-math.
+ *
+ * Parity status: every function here is pinned by tests against the paper's
+ * worked example, closed forms, invariants, library routines or brute force,
+ * except the items the paper leaves unpinned (H15 log-sum-exp, per-tile
+ * element values, FP8 P rounding), which are pinned only by the definitions
+ * written out below.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+enum { OR_BF16 = 0, OR_FP8_E4M3 = 1 };
+enum {
+    OR_EXACT = 0,        /* App. A.1 exact softmax attention, fp64 */
+    OR_H15_TILE = 1,     /* Rowmax-H15 with the per-tile running max (App. B.2) */
+    OR_H15_WHOLEROW = 2, /* Rowmax-H15 anchored at the final whole-row max */
+    OR_ROWMAX_POT = 3,   /* App. A.6 Rowmax-PoT, whole row, K_max = 20 */
+    OR_EXACT_TILE = 4    /* diagnostic: exact exp2 inside the same tile loop,
+                            with the kernel's P storage rounding */
+};
+
+static uint32_t f2u(float f) { uint32_t u; memcpy(&u, &f, 4); return u; }
+static float u2f(uint32_t u) { float f; memcpy(&f, &u, 4); return f; }
+
+int oracle_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* ---- operand decoding ------------------------------------------------- */
+
+/* bfloat16: the top 16 bits of an IEEE binary32 pattern. */
+double oracle_bf16_value(uint16_t b) { return (double)u2f((uint32_t)b << 16); }
+
+/* OCP E4M3 ("e4m3fn"): sign, 4 exponent bits with bias 7, 3 mantissa bits,
+ * subnormals at exponent field 0, no infinities, S.1111.111 is NaN. */
+double oracle_e4m3_value(uint8_t c)
+{
+    int s = c >> 7, e = (c >> 3) & 15, m = c & 7;
+    double v;
+    if (e == 15 && m == 7) return NAN;
+    if (e == 0) v = ldexp((double)m / 8.0, -6);
+    else v = ldexp(1.0 + (double)m / 8.0, e - 7);
+    return s ? -v : v;
+}
+
+/* Round to the nearest finite E4M3 value, ties to the code with an even
+ * mantissa, saturating at +-448.  Brute force over every finite code. */
+uint8_t oracle_e4m3_rne_satfinite(double x)
+{
+    if (isnan(x)) return 0x7F;
+    uint8_t sign = signbit(x) ? 0x80 : 0x00;
+    double a = fabs(x);
+    if (a >= 448.0) return sign | 0x7E;
+    int best = 0;
+    double bestd = INFINITY;
+    for (int c = 0; c <= 0x7E; c++) {
+        double dd = fabs(oracle_e4m3_value((uint8_t)c) - a);
+        if (dd < bestd || (dd == bestd && (c & 1) == 0)) { best = c; bestd = dd; }
+    }
+    return sign | (uint8_t)best;
+}
+
+/* Round an fp32 value to bfloat16 (round to nearest, ties to even). */
+static uint16_t bf16_rne(float f)
+{
+    uint32_t u = f2u(f);
+    uint32_t lsb = (u >> 16) & 1u;
+    return (uint16_t)((u + 0x7FFFu + lsb) >> 16);
+}
+
+/* ---- the Rowmax-H15 weight -------------------------------------------- */
+
+/* App. B.1 "Implementation".  y is the doubled base-two exponent 2x in FP32.
+ * Clamp at -252 (so the exponent field cannot wrap), add 0x4B400000 =
+ * 2^23 + 2^22 with an FP32 round-to-nearest-even add (this leaves
+ * n = RNE(y) in the low mantissa bits), shift left by 22 (bit 0 of n becomes
+ * the leading mantissa bit, the rest lands in the exponent field) and add the
+ * bit pattern of 1.0, all modulo 2^32. */
+float oracle_h15_weight(float y)
+{
+    volatile float yc = (y < -252.0f) ? -252.0f : y;
+    volatile float t = yc + 12582912.0f; /* 0x4B400000 as a float */
+    uint32_t u = (f2u(t) << 22) + 0x3F800000u;
+    return u2f(u);
+}
+
+/* Sec. 5.2 Eq. (m-h15) written out with library rounding: n = RNE(2x),
+ * weight = (1 + (n mod 2)/2) * 2^floor(n/2), floor toward -inf and the
+ * non-negative residue.  The argument is y = 2x. */
+double oracle_h15_ideal(double y)
+{
+    double n = nearbyint(y); /* default rounding mode: nearest, ties to even */
+    double k = floor(n / 2.0);
+    double r = n - 2.0 * k;
+    return (1.0 + 0.5 * r) * ldexp(1.0, (int)k);
+}
+
+/* Exhaustive comparison of the two forms above over every fp32 y in
+ * [lo, hi], both taken after the clamp at -252.  Returns the number of
+ * mismatching bit patterns; *count receives the number of values tested. */
+int64_t oracle_h15_exhaustive(float lo, float hi, int64_t* count)
+{
+    int64_t bad = 0, n = 0;
+    /* positive half: patterns 0x00000000 .. bits(hi); negative half:
+     * 0x80000000 .. bits(lo).  Walk both ranges of integer patterns. */
+    uint32_t hi_bits = hi >= 0 ? f2u(hi) : 0;
+    uint32_t lo_mag = lo <= 0 ? (f2u(lo) & 0x7FFFFFFFu) : 0;
+    int64_t npos = hi >= 0 ? (int64_t)hi_bits + 1 : 0;
+    int64_t nneg = lo <= 0 ? (int64_t)lo_mag + 1 : 0;
+    int64_t total = npos + nneg;
+#pragma omp parallel for reduction(+ : bad, n) schedule(static)
+    for (int64_t idx = 0; idx < total; idx++) {
+        uint32_t bits = idx < npos ? (uint32_t)idx : (0x80000000u | (uint32_t)(idx - npos));
+        float y = u2f(bits);
+        if (y < lo || y > hi) continue;
+        double yc = y < -252.0f ? -252.0 : (double)y;
+        float want = (float)oracle_h15_ideal(yc);
+        float got = oracle_h15_weight(y);
+        n++;
+        if (f2u(want) != f2u(got)) bad++;
+    }
+    if (count) *count = n;
+    return bad;
+}
+
+/* The exponent-path constant: the base-two scale applied to a raw logit,
+ * c1 = fp32(scale * q_descale * k_descale * log2(e)), products taken in
+ * double in this order.  The H15 path uses c2 = 2*c1 (App. B.1: separate,
+ * doubled exponent-path constants). */
+float oracle_c1(double scale, double qd, double kd)
+{
+    return (float)(scale * qd * kd * 1.4426950408889634);
+}
+
+/* ---- one row of the tiled online-softmax recurrence -------------------- */
+
+/* Rowmax-H15 (or the exact-exp2 diagnostic) for one query row, following
+ * App. B.1 / B.2: keys are visited in tiles of Bc in increasing order; for
+ * each tile the running max m is moved to m_new (threshold tau in base-two
+ * units; tau = 0 always moves it to max(m, tile max)); the running sum and
+ * the output accumulator are rescaled by alpha = 2^((m - m_new) c1); the
+ * weight of each valid key is computed from the doubled exponent
+ * y = fma(s, c2, fma(-m_new, c2, 2 off)), and the row sum and PV consume the
+ * same weights (P is W stored in the operand type).  Masked keys carry
+ * W = P = 0 and never enter the max.
+ *   s      fp32 raw logits of the row, length S
+ *   vrows  decoded V rows [S][d] (NULL: no O accumulation)
+ *   jend   number of valid keys (keys 0 .. jend-1), >= 1
+ * Outputs (each optional): o[d] (unscaled by vd), *lse, w[S], p[S]. */
+static void tiled_row(const float* s, const double* vrows, int S, int d, int jend, float c1,
+                      int off, int Bc, double tau, int dtype, int exact_exp, double vd,
+                      double* o, double* lse, float* w, uint32_t* p, double* acc)
+{
+    const float c2 = 2.0f * c1; /* exact doubling */
+    float m = -INFINITY;
+    double l = 0.0;
+    if (acc) for (int c = 0; c < d; c++) acc[c] = 0.0;
+    for (int j = 0; j < S; j++) {
+        if (w) w[j] = 0.0f;
+        if (p) p[j] = 0u;
+    }
+    for (int t0 = 0; t0 < S && t0 < jend; t0 += Bc) {
+        int t1 = t0 + Bc < S ? t0 + Bc : S;
+        int v1 = t1 < jend ? t1 : jend;
+        float mt = -INFINITY;
+        for (int j = t0; j < v1; j++) mt = fmaxf(mt, s[j]);
+        float m_new;
+        if (m == -INFINITY) m_new = mt;
+        else m_new = (((double)mt - (double)m) * (double)c1 > tau) ? fmaxf(m, mt) : m;
+        double alpha = (m == -INFINITY) ? 0.0 : exp2(((double)m - (double)m_new) * (double)c1);
+        l *= alpha;
+        if (acc) for (int c = 0; c < d; c++) acc[c] *= alpha;
+        float nb2 = fmaf(-m_new, c2, (float)(2 * off));
+        float nb1 = fmaf(-m_new, c1, (float)off);
+        for (int j = t0; j < v1; j++) {
+            float wj;
+            if (exact_exp) wj = (float)exp2((double)fmaf(s[j], c1, nb1));
+            else wj = oracle_h15_weight(fmaf(s[j], c2, nb2));
+            uint32_t pb;
+            double pv;
+            if (dtype == OR_BF16) {
+                pb = bf16_rne(wj);
+                pv = oracle_bf16_value((uint16_t)pb);
+            } else {
+                pb = oracle_e4m3_rne_satfinite((double)wj);
+                pv = oracle_e4m3_value((uint8_t)pb);
+            }
+            l += (double)wj;
+            if (acc && vrows)
+                for (int c = 0; c < d; c++) acc[c] += pv * vrows[(size_t)j * d + c];
+            if (w) w[j] = wj;
+            if (p) p[j] = pb;
+        }
+        m = m_new;
+    }
+    if (o && acc)
+        for (int c = 0; c < d; c++) o[c] = acc[c] / l * vd;
+    if (lse) *lse = M_LN2 * ((double)m * (double)c1 + log2(l) - (double)off);
+}
+
+/* W and P of one row from given fp32 logits (for bit-exact comparison with
+ * values that another implementation stored for the same logits). */
+int oracle_h15_row_from_logits(const float* s, int S, int i, int causal, float c1, int dtype,
+                               int Bc, double tau, int exact_exp, float* w_out, uint32_t* p_out,
+                               double* lse_out)
+{
+    if (S <= 0 || Bc <= 0 || i < 0 || i >= S) return -1;
+    int off = dtype == OR_FP8_E4M3 ? 8 : 0;
+    int jend = causal ? i + 1 : S;
+    tiled_row(s, NULL, S, 0, jend, c1, off, Bc, tau, dtype, exact_exp, 1.0, NULL, lse_out, w_out,
+              p_out, NULL);
+    return 0;
+}
+
+/* ---- full attention --------------------------------------------------- */
+
+static double decode(const void* base, size_t idx, int dtype)
+{
+    if (dtype == OR_BF16) return oracle_bf16_value(((const uint16_t*)base)[idx]);
+    return oracle_e4m3_value(((const uint8_t*)base)[idx]);
+}
+
+/* Attention forward for the listed rows (flat index (b*Hq + h)*S + i), or
+ * for all B*Hq*S rows when rows == NULL.  q: [B][Hq][S][d]; k, v:
+ * [B][Hkv][S][d], stored as bf16 bit patterns (uint16) or e4m3 codes
+ * (uint8).  Query head h reads key/value head h / (Hq/Hkv).  Causal means
+ * query i sees keys j <= i.  o receives nrows x d doubles, lse nrows
+ * doubles (natural log of the normaliser of the scaled logits).
+ * Returns 0, or -1 on invalid arguments. */
+int oracle_attn(const void* q, const void* k, const void* v, int dtype, double qd, double kd,
+                double vd, int B, int Hq, int Hkv, int S, int d, int causal, double scale, int mode,
+                int Bc, double tau, const int64_t* rows, int64_t nrows, double* o, double* lse)
+{
+    if (!q || !k || !v || !o || B <= 0 || Hq <= 0 || Hkv <= 0 || S <= 0 || d <= 0) return -1;
+    if (Hq % Hkv != 0 || (dtype != OR_BF16 && dtype != OR_FP8_E4M3) || mode < 0 || mode > 4)
+        return -1;
+    if ((mode == OR_H15_TILE || mode == OR_EXACT_TILE) && Bc <= 0) return -1;
+    const int64_t total = (int64_t)B * Hq * S;
+    if (!rows) nrows = total;
+    const int group = Hq / Hkv;
+    const double sigma = scale * qd * kd; /* natural-log scale of a raw logit */
+    const float c1 = oracle_c1(scale, qd, kd);
+    const int off = dtype == OR_FP8_E4M3 ? 8 : 0;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 4) reduction(| : bad)
+    for (int64_t r = 0; r < nrows; r++) {
+        int64_t flat = rows ? rows[r] : r;
+        if (flat < 0 || flat >= total) { bad = 1; continue; }
+        const int i = (int)(flat % S);
+        const int h = (int)((flat / S) % Hq);
+        const int b = (int)(flat / ((int64_t)S * Hq));
+        const int hk = h / group;
+        const size_t qoff = (((size_t)b * Hq + h) * S + i) * d;
+        const size_t kvoff = ((size_t)b * Hkv + hk) * S * d;
+        const int jend = causal ? i + 1 : S;
+
+        double* qrow = malloc(sizeof(double) * d);
+        double* sexact = malloc(sizeof(double) * S);
+        double* vrows = malloc(sizeof(double) * (size_t)jend * d);
+        double* acc = malloc(sizeof(double) * d);
+        float* s32 = malloc(sizeof(float) * S);
+        for (int c = 0; c < d; c++) qrow[c] = decode(q, qoff + c, dtype);
+        for (int j = 0; j < jend; j++) {
+            double dot = 0.0;
+            for (int c = 0; c < d; c++) dot += qrow[c] * decode(k, kvoff + (size_t)j * d + c, dtype);
+            sexact[j] = dot;
+            s32[j] = (float)dot; /* the raw logit, rounded once to fp32 */
+            for (int c = 0; c < d; c++) vrows[(size_t)j * d + c] = decode(v, kvoff + (size_t)j * d + c, dtype);
+        }
+        for (int j = jend; j < S; j++) s32[j] = 0.0f; /* never read: masked */
+        double* orow = o + (size_t)r * d;
+
+        if (mode == OR_EXACT || mode == OR_ROWMAX_POT) {
+            double smax = -INFINITY;
+            for (int j = 0; j < jend; j++) smax = fmax(smax, sexact[j]);
+            double den = 0.0;
+            for (int c = 0; c < d; c++) acc[c] = 0.0;
+            for (int j = 0; j < jend; j++) {
+                double wj;
+                if (mode == OR_EXACT) {
+                    wj = exp(-sigma * (smax - sexact[j])); /* w_j = exp(-Delta_j) */
+                } else {
+                    double xj = sigma * (smax - sexact[j]) / M_LN2; /* x_j = Delta_j / ln 2 */
+                    double dj = floor(xj + 0.5);
+                    if (dj > 20.0) dj = 20.0; /* K_max = 20 */
+                    wj = ldexp(1.0, -(int)dj);
+                }
+                den += wj;
+                for (int c = 0; c < d; c++) acc[c] += wj * vrows[(size_t)j * d + c];
+            }
+            for (int c = 0; c < d; c++) orow[c] = acc[c] / den * vd;
+            if (lse) lse[r] = sigma * smax + log(den);
+        } else {
+            int tile = (mode == OR_H15_WHOLEROW) ? S : Bc;
+            tiled_row(s32, vrows, S, d, jend, c1, off, tile, tau, dtype, mode == OR_EXACT_TILE, vd,
+                      orow, lse ? &lse[r] : NULL, NULL, NULL, acc);
+        }
+        free(qrow); free(sexact); free(vrows); free(acc); free(s32);
+    }
+    return bad ? -1 : 0;
+}
+
+/* Raw fp32 logits s_ij = fp32(sum_c q_ic k_jc) of one query row (exact fp64
+ * sum of the decoded operands, rounded once).  Keys j > i are still written
+ * (the caller decides about masking). */
+int oracle_logits_row(const void* q, const void* k, int dtype, int B, int Hq, int Hkv, int S, int d,
+                      int b, int h, int i, float* s_out)
+{
+    if (!q || !k || !s_out || b < 0 || b >= B || h < 0 || h >= Hq || i < 0 || i >= S) return -1;
+    if (Hkv <= 0 || Hq % Hkv) return -1;
+    const int hk = h / (Hq / Hkv);
+    const size_t qoff = (((size_t)b * Hq + h) * S + i) * d;
+    const size_t kvoff = ((size_t)b * Hkv + hk) * S * d;
+    for (int j = 0; j < S; j++) {
+        double dot = 0.0;
+        for (int c = 0; c < d; c++)
+            dot += decode(q, qoff + c, dtype) * decode(k, kvoff + (size_t)j * d + c, dtype);
+        s_out[j] = (float)dot;
+    }
+    return 0;
+}
