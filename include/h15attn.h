@@ -1,0 +1,113 @@
+/*
+ * h15attn: fused attention forward for AMD Instinct MI355X (gfx950) whose
+ * softmax exponential is either the hardware exp2 (the control) or
+ * Rowmax-H15, from "Approximating Softmax in Pretrained LLMs: Model
+ * Sensitivity and Kernel Acceleration".
+ *
+ * Operation (App. A.1, Eq. (exact-attention), with the valid key set V(i) =
+ * {j : j <= i} when causal, else every key):
+ *     O[b,h,i,:] = sum_{j in V(i)} p_ij V[b,h/G,j,:],   G = Hq / Hkv,
+ *     p_ij = w_ij / sum_{j in V(i)} w_ij,
+ * computed online over key tiles of attn_tile_bc() keys with a running row
+ * maximum m (FlashAttention-style).  The weight w_ij is
+ *   ATTN_EXP_EXACT: exp2(c1 * (s_ij - m) + off), hardware exp2;
+ *   ATTN_EXP_H15:   Rowmax-H15 of the base-two exponent x = c1*(s_ij - m)
+ *                   + off (Sec. 5.2 Eq. (m-h15); App. B.1 "Implementation"):
+ *                   n = RNE(2x), w = (1 + (n mod 2)/2) * 2^floor(n/2),
+ *                   realised as y = fma(s, c2, fma(-m, c2, 2 off)),
+ *                   y = max(y, -252), t = y + 0x1.8p23f (RNE),
+ *                   w = bits^-1((bits(t) << 22) + bits(1.0f)), c2 = 2*c1.
+ * where s_ij = sum_c q_ic k_jc is the raw logit of the stored operands (bf16
+ * values, or e4m3 values without their descales) accumulated in fp32,
+ * c1 = fp32(scale * q_descale * k_descale * log2(e)) (products in double,
+ * in that order), off = 0 for BF16 and 8 for FP8 (so P = w <= 2^8 fits
+ * e4m3), and m the running maximum of the raw logits, moved at every key
+ * tile to the maximum so far (rescale threshold 0, App. B.2: per-tile
+ * running max).  The row sum and the PV product consume the same weights:
+ * l sums w in fp32; PV multiplies V by P = w stored as bf16 (exact for H15)
+ * or e4m3 (round to nearest even).  Output:
+ *     O = (sum_j P_j V_j) / l * v_descale, stored as bf16;
+ *     LSE = ln2 * (m * c1 + log2(l) - off)   (natural log of the normaliser
+ *           of the scaled logits; for H15 the approximated normaliser).
+ *
+ * Layouts: every tensor is contiguous BHSD (batch, head, sequence, head
+ * dim).  q: [B][Hq][S][d]; k, v: [B][Hkv][S][d]; o: [B][Hq][S][d] bf16;
+ * lse: [B][Hq][S] fp32 (may be NULL).  Elements are bf16 (2 bytes) or OCP
+ * e4m3fn (1 byte) according to dtype.  Query head h reads key/value head
+ * h / (Hq / Hkv).  Causal masking is top-left aligned (query i sees keys
+ * j <= i).
+ *
+ * Memory and streams: all pointers are device pointers owned by the caller;
+ * the library allocates, frees and synchronises nothing.  Calls are
+ * asynchronous on the given stream (NULL: the default stream); buffers must
+ * stay valid until the stream reaches the work.  The library holds no state
+ * and may be called from several threads.
+ *
+ * Errors: arguments are validated before anything is launched; on error
+ * nothing is written.  Every entry point returns ATTN_OK or a negative code,
+ * described by attn_strerror().
+ */
+#ifndef H15ATTN_H
+#define H15ATTN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum attn_dtype { ATTN_BF16 = 0, ATTN_FP8_E4M3 = 1 };
+enum attn_expmode { ATTN_EXP_EXACT = 0, ATTN_EXP_H15 = 1 };
+enum attn_status {
+    ATTN_OK = 0,
+    ATTN_EINVAL = -1,      /* null pointer, non-positive size, Hq % Hkv != 0,
+                              scale or descale not positive and finite */
+    ATTN_EUNSUPPORTED = -2, /* d not in {64, 128}, unknown dtype or exp_mode,
+                              pointer not 16-byte aligned */
+    ATTN_ELAUNCH = -3      /* the HIP launch reported an error */
+};
+
+/* Optional per-call settings.  FP8 requires the three per-tensor descales
+ * (the factors that turn stored e4m3 values back into real values); BF16
+ * ignores them.  stream is a hipStream_t (NULL: default stream). */
+typedef struct attn_opts {
+    float q_descale, k_descale, v_descale;
+    void* stream;
+} attn_opts;
+
+/* Attention forward on the default stream with unit descales. */
+int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq,
+             int Hkv, int S, int d, int causal, float scale, int dtype, int exp_mode);
+
+/* Attention forward with descales and a stream (opts may be NULL for BF16). */
+int attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq,
+                int Hkv, int S, int d, int causal, float scale, int dtype, int exp_mode,
+                const attn_opts* opts);
+
+/* Test access to the method's intermediate values.  Runs the same kernel code
+ * as attn_fwd_ex (same tiles, same arithmetic, O and LSE written identically)
+ * and, for query rows [row0, row0 + nrows) of head (b, h), also stores the
+ * fp32 raw logits s, the fp32 weights w and the stored P bits (bf16 pattern
+ * or e4m3 code, zero-extended) of every key: s_out, w_out, p_bits_out are
+ * device buffers of nrows * S elements, row-major.  Entries of masked keys
+ * are written as s = -inf, w = 0, P = 0.  The weight stored is the one
+ * computed at the key's tile, relative to the running maximum of that time
+ * (before later rescales).  Requires 0 <= row0, nrows >= 1,
+ * row0 + nrows <= S, 0 <= b < B, 0 <= h < Hq; otherwise ATTN_EINVAL. */
+int attn_fwd_probe(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq,
+                   int Hkv, int S, int d, int causal, float scale, int dtype, int exp_mode,
+                   const attn_opts* opts, int b, int h, int row0, int nrows, float* s_out,
+                   float* w_out, uint32_t* p_bits_out);
+
+/* Static description of an error code. */
+const char* attn_strerror(int code);
+
+/* Key-tile width of the online recurrence (the running maximum moves once per
+ * tile of this many keys, in increasing key order). */
+int attn_tile_bc(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* H15ATTN_H */

@@ -1,0 +1,156 @@
+"""Rowmax-H15 fused attention forward for MI355X (gfx950).
+
+A thin ctypes binding over ``libh15attn.so`` (built from ``csrc/h15attn.hip``
+by ``build.py``).  Every step of the attention runs in the HIP kernels; this
+module only marshals torch tensors (device memory and streams) into the C ABI
+declared in ``include/h15attn.h``.  The functions carry the C names.
+
+There is no fallback: if the library is missing or a call fails, an exception
+is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+from pathlib import Path
+
+_PKG = Path(__file__).resolve().parent
+LIB_PATH = _PKG / "libh15attn.so"
+
+ATTN_BF16, ATTN_FP8_E4M3 = 0, 1
+ATTN_EXP_EXACT, ATTN_EXP_H15 = 0, 1
+ATTN_OK, ATTN_EINVAL, ATTN_EUNSUPPORTED, ATTN_ELAUNCH = 0, -1, -2, -3
+
+# every symbol the header declares
+EXPORTS = ("attn_fwd", "attn_fwd_ex", "attn_fwd_probe", "attn_strerror", "attn_tile_bc")
+
+
+class attn_opts(ctypes.Structure):
+    _fields_ = [("q_descale", ctypes.c_float), ("k_descale", ctypes.c_float),
+                ("v_descale", ctypes.c_float), ("stream", ctypes.c_void_p)]
+
+
+class AttnError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        super().__init__(f"{where}: {attn_strerror(code)} ({code})")
+        self.code = code
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libh15attn.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not LIB_PATH.exists():
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2609_33586_amd.build.build()")
+    L = ctypes.CDLL(str(LIB_PATH))
+    P, I, F = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
+    common = [P, P, P, P, P, I, I, I, I, I, I, F, I, I]
+    L.attn_fwd.argtypes = common
+    L.attn_fwd.restype = I
+    L.attn_fwd_ex.argtypes = common + [ctypes.POINTER(attn_opts)]
+    L.attn_fwd_ex.restype = I
+    L.attn_fwd_probe.argtypes = common + [ctypes.POINTER(attn_opts), I, I, I, I, P, P, P]
+    L.attn_fwd_probe.restype = I
+    L.attn_strerror.argtypes = [I]
+    L.attn_strerror.restype = ctypes.c_char_p
+    L.attn_tile_bc.argtypes = []
+    L.attn_tile_bc.restype = I
+    _lib = L
+    return L
+
+
+def attn_strerror(code: int) -> str:
+    return lib().attn_strerror(int(code)).decode()
+
+
+def attn_tile_bc() -> int:
+    return int(lib().attn_tile_bc())
+
+
+def _dtype_of(t) -> int:
+    import torch
+    if t.dtype in (torch.bfloat16, torch.uint16, torch.int16):
+        return ATTN_BF16
+    if t.dtype in (torch.float8_e4m3fn, torch.uint8):
+        return ATTN_FP8_E4M3
+    raise TypeError(f"unsupported operand dtype {t.dtype}")
+
+
+def _check(q, k, v):
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if not t.is_cuda or not t.is_contiguous() or t.dim() != 4:
+            raise ValueError(f"{name} must be a contiguous 4-D device tensor [B,H,S,d]")
+    B, Hq, S, d = q.shape
+    Hkv = k.shape[1]
+    if tuple(k.shape) != (B, Hkv, S, d) or tuple(v.shape) != (B, Hkv, S, d):
+        raise ValueError("k and v must be [B,Hkv,S,d] with q's B, S, d")
+    dt = _dtype_of(q)
+    if _dtype_of(k) != dt or _dtype_of(v) != dt:
+        raise TypeError("q, k, v must share one operand type")
+    return B, Hq, Hkv, S, d, dt
+
+
+def _outputs(q, out, lse, want_lse):
+    import torch
+    B, Hq, S, d = q.shape
+    if out is None:
+        out = torch.empty((B, Hq, S, d), dtype=torch.bfloat16, device=q.device)
+    if lse is None and want_lse:
+        lse = torch.empty((B, Hq, S), dtype=torch.float32, device=q.device)
+    return out, lse
+
+
+def _opts(descale, stream):
+    import torch
+    qd, kd, vd = descale if descale is not None else (1.0, 1.0, 1.0)
+    st = stream if stream is not None else torch.cuda.current_stream()
+    return attn_opts(float(qd), float(kd), float(vd), ctypes.c_void_p(st.cuda_stream))
+
+
+def attn_fwd_ex(q, k, v, *, causal: bool, scale: float, exp_mode: int, descale=None, stream=None,
+                out=None, lse=None, want_lse: bool = True):
+    """O (and LSE) of attention; see include/h15attn.h for the definition."""
+    B, Hq, Hkv, S, d, dt = _check(q, k, v)
+    out, lse = _outputs(q, out, lse, want_lse)
+    opts = _opts(descale, stream)
+    rc = lib().attn_fwd_ex(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                           lse.data_ptr() if lse is not None else None, B, Hq, Hkv, S, d,
+                           int(bool(causal)), float(scale), dt, int(exp_mode), ctypes.byref(opts))
+    if rc != ATTN_OK:
+        raise AttnError(rc, "attn_fwd_ex")
+    return out, lse
+
+
+def attn_fwd(q, k, v, *, causal: bool, scale: float, exp_mode: int, out=None, lse=None,
+             want_lse: bool = True):
+    """attn_fwd on the default stream with unit descales."""
+    B, Hq, Hkv, S, d, dt = _check(q, k, v)
+    out, lse = _outputs(q, out, lse, want_lse)
+    rc = lib().attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                        lse.data_ptr() if lse is not None else None, B, Hq, Hkv, S, d,
+                        int(bool(causal)), float(scale), dt, int(exp_mode))
+    if rc != ATTN_OK:
+        raise AttnError(rc, "attn_fwd")
+    return out, lse
+
+
+def attn_fwd_probe(q, k, v, *, causal: bool, scale: float, exp_mode: int, b: int, h: int,
+                   row0: int, nrows: int, descale=None, stream=None):
+    """Returns (O, LSE, s, w, p_bits) with s/w/p_bits of shape [nrows, S]."""
+    import torch
+    B, Hq, Hkv, S, d, dt = _check(q, k, v)
+    out, lse = _outputs(q, None, None, True)
+    s = torch.empty((nrows, S), dtype=torch.float32, device=q.device)
+    w = torch.empty((nrows, S), dtype=torch.float32, device=q.device)
+    pb = torch.empty((nrows, S), dtype=torch.int32, device=q.device)
+    opts = _opts(descale, stream)
+    rc = lib().attn_fwd_probe(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
+                              B, Hq, Hkv, S, d, int(bool(causal)), float(scale), dt, int(exp_mode),
+                              ctypes.byref(opts), int(b), int(h), int(row0), int(nrows),
+                              s.data_ptr(), w.data_ptr(), pb.data_ptr())
+    if rc != ATTN_OK:
+        raise AttnError(rc, "attn_fwd_probe")
+    return out, lse, s, w, pb

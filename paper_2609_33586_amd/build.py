@@ -1,0 +1,52 @@
+"""Build the gfx950 library ``libh15attn.so`` in-tree with hipcc.
+
+Flags that matter:
+  * ``-ffp-contract=off``: the H15 exponent argument must be computed by the
+    fused multiply-adds written in the source and nothing else (bit-exact
+    weights), and no other expression may be contracted behind our back;
+  * ``-Xclang -target-feature -Xclang -packed-fp32-ops``: no packed fp32 VALU
+    instructions are generated (the host pass warns that it does not know the
+    feature; that is harmless).
+"""
+from __future__ import annotations
+
+import os
+import subprocess
+import sys
+from pathlib import Path
+
+PKG = Path(__file__).resolve().parent
+ROOT = PKG.parent
+SRC = PKG / "csrc" / "h15attn.hip"
+INCLUDE = ROOT / "include"
+LIB_PATH = PKG / "libh15attn.so"
+ARCH = "gfx950"
+
+HIPCC_FLAGS = [
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-shared", "-fPIC",
+    "-ffp-contract=off", "-fno-fast-math",
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wall", "-Wno-unused-function",
+]
+
+
+def hipcc() -> str:
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    return str(Path(rocm) / "bin" / "hipcc")
+
+
+def build(extra: list[str] | None = None, verbose: bool = False) -> Path:
+    tmp = LIB_PATH.with_name(LIB_PATH.name + ".tmp")
+    cmd = [hipcc(), *HIPCC_FLAGS, *(extra or []), f"-I{INCLUDE}", str(SRC), "-o", str(tmp)]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        sys.stderr.write(res.stdout + res.stderr)
+        raise RuntimeError(f"hipcc failed ({res.returncode}) building {SRC.name}")
+    if verbose:
+        sys.stderr.write(res.stderr)
+    tmp.replace(LIB_PATH)
+    return LIB_PATH
+
+
+if __name__ == "__main__":
+    print(build(verbose="-v" in sys.argv))

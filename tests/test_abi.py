@@ -1,0 +1,76 @@
+"""The C ABI without a GPU: the library loads, exports every function the
+header declares, and rejects invalid arguments before touching the GPU."""
+import ctypes
+import math
+import re
+from pathlib import Path
+
+import pytest
+
+import paper_2609_33586_amd as pkg
+
+HEADER = Path(__file__).resolve().parent.parent / "include" / "h15attn.h"
+
+
+def declared_functions():
+    text = re.sub(r"/\*.*?\*/", "", HEADER.read_text(), flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\**\s+\**(attn_\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not pkg.LIB_PATH.exists():
+        from paper_2609_33586_amd import build
+        build.build()
+    return pkg.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = declared_functions()
+    assert set(names) == set(pkg.EXPORTS)
+    for n in names:
+        assert hasattr(L, n)
+
+
+def test_tile_and_strerror(L):
+    assert pkg.attn_tile_bc() == 128
+    assert pkg.attn_strerror(0) == "ok"
+    for c in (-1, -2, -3, 7):
+        assert isinstance(pkg.attn_strerror(c), str) and pkg.attn_strerror(c)
+
+
+FAKE = 0x100000  # a 16-byte aligned address that is never dereferenced on error
+
+
+def call(L, q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, B=1, Hq=2, Hkv=1, S=64, d=128, causal=0,
+         scale=0.1, dtype=0, mode=1, opts=None):
+    if opts is None:
+        return L.attn_fwd_ex(q, k, v, o, lse, B, Hq, Hkv, S, d, causal, scale, dtype, mode, None)
+    return L.attn_fwd_ex(q, k, v, o, lse, B, Hq, Hkv, S, d, causal, scale, dtype, mode, ctypes.byref(opts))
+
+
+def test_invalid_arguments(L):
+    E_INV, E_UNS = pkg.ATTN_EINVAL, pkg.ATTN_EUNSUPPORTED
+    assert call(L, q=None) == E_INV
+    assert call(L, o=None) == E_INV
+    for kw in ({"B": 0}, {"Hq": 0}, {"Hkv": 0}, {"S": 0}, {"S": -5}, {"d": 0}):
+        assert call(L, **kw) == E_INV
+    assert call(L, Hq=3, Hkv=2) == E_INV
+    for sc in (0.0, -1.0, math.inf, math.nan):
+        assert call(L, scale=sc) == E_INV
+    assert call(L, d=96) == E_UNS and call(L, d=256) == E_UNS
+    assert call(L, dtype=2) == E_UNS and call(L, mode=5) == E_UNS
+    assert call(L, q=FAKE + 8) == E_UNS
+    assert call(L, lse=FAKE + 2) == E_UNS
+    # FP8 needs positive finite descales
+    assert call(L, dtype=1) == E_INV
+    for bad in ((0.0, 1.0, 1.0), (1.0, -1.0, 1.0), (1.0, 1.0, math.inf)):
+        assert call(L, dtype=1, opts=pkg.attn_opts(*bad, None)) == E_INV
+
+
+def test_probe_invalid_rows(L):
+    opts = pkg.attn_opts(1.0, 1.0, 1.0, None)
+    args = [FAKE, FAKE, FAKE, FAKE, None, 1, 2, 1, 64, 128, 0, 0.1, 0, 1, ctypes.byref(opts)]
+    for b, h, r0, n in ((1, 0, 0, 1), (0, 2, 0, 1), (0, 0, -1, 1), (0, 0, 0, 0), (0, 0, 60, 5)):
+        assert L.attn_fwd_probe(*args, b, h, r0, n, FAKE, FAKE, FAKE) == pkg.ATTN_EINVAL
+    assert L.attn_fwd_probe(*args, 0, 0, 0, 4, None, FAKE, FAKE) == pkg.ATTN_EINVAL
