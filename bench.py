@@ -1,0 +1,186 @@
+"""Benchmark: Rowmax-H15 fused attention forward on one MI355X.
+
+One step = one attention forward (the whole hot path: QK^T, online softmax
+with the Rowmax-H15 weight, PV, epilogue) over the workload's synthetic
+inputs, already resident in HBM.  The exact-exp2 variant of the same kernel is
+timed the same way, in alternating rounds, as the control.
+
+Prints ONE JSON line.  value = effective TFLOP/s of the H15 forward (FLOPs in
+the FlashAttention convention: 4 B Hq S^2 d, halved when causal).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+from pathlib import Path
+
+import numpy as np
+
+ROOT = Path(__file__).resolve().parent
+sys.path.insert(0, str(ROOT))
+
+DEFAULT_WORKLOAD = "causal_fp8_b2_h32kv8_s8192_d128_sharp"
+# MI355X published dense peaks (TFLOP/s)
+PEAK = {"bf16": 2500.0, "fp8_e4m3": 5000.0}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--rounds", type=int, default=3)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU baseline sample time")
+    ap.add_argument("--modes", default="h15,exact")
+    ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
+                    help="only run a plain device-to-device copy of this many GiB (5 times), "
+                         "the reference for scaling HBM byte counters")
+    return ap.parse_args()
+
+
+def cpu_baseline(w, inp, scale, target_s):
+    """The CPU oracle (as it stands) on a bounded sample of query rows."""
+    import oracle
+
+    rng = np.random.default_rng(0)
+    total_rows = w.B * w.Hq * w.S
+    n = 16
+    spent = 0.0
+    rows_done = 0
+    flops_done = 0.0
+    while True:
+        rows = np.sort(rng.choice(total_rows, size=min(n, total_rows), replace=False))
+        t0 = time.perf_counter()
+        oracle.attn(inp.q, inp.k, inp.v, dtype=inp.dtype, causal=w.causal, scale=scale, mode=oracle.H15_TILE,
+                    descale=inp.descale, Bc=128, rows=rows)
+        dt = time.perf_counter() - t0
+        i = rows % w.S
+        keys = (i + 1) if w.causal else np.full_like(i, w.S)
+        spent += dt
+        rows_done += len(rows)
+        flops_done += float(np.sum(4.0 * keys * w.d))
+        if spent >= target_s or n >= total_rows:
+            break
+        n = int(min(total_rows, max(n * 2, n * target_s / max(dt, 1e-3) * 0.6)))
+    return {"value": flops_done / spent / 1e12, "unit": "TFLOP/s", "cores": oracle.threads(), "kind": "oracle",
+            "sample": f"{rows_done} random query rows of the workload (H15 per-tile mode), {spent:.1f} s; "
+                      f"FLOPs counted per row as 4*keys*d"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: the attention forward is timed on a single MI355X "
+              f"(--gpus {args.gpus} is not supported; head/batch sharding across GPUs needs no "
+              f"communication and is described in DESIGN.md).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    if args.copy_calibration > 0:
+        n = int(args.copy_calibration * (1 << 30))
+        src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n, "copies": 5}), flush=True)
+        return
+
+    import paper_2609_33586_amd as pkg
+    from paper_2609_33586_amd import synth
+
+    w = synth.WORKLOADS[args.workload]
+    inp = synth.workload_inputs(w)
+    dev = torch.device("cuda:0")
+    if w.dtype == synth.BF16:
+        q, k, v = (torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16) for x in (inp.q, inp.k, inp.v))
+        dtname = "bf16"
+    else:
+        q, k, v = (torch.from_numpy(x).to(dev).view(torch.float8_e4m3fn) for x in (inp.q, inp.k, inp.v))
+        dtname = "fp8_e4m3"
+    scale = float(np.float32(1.0 / math.sqrt(w.d)))
+    out = torch.empty((w.B, w.Hq, w.S, w.d), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((w.B, w.Hq, w.S), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    modes = {"h15": pkg.ATTN_EXP_H15, "exact": pkg.ATTN_EXP_EXACT}
+    want = [m for m in args.modes.split(",") if m in modes]
+
+    def call(mode):
+        pkg.attn_fwd_ex(q, k, v, causal=w.causal, scale=scale, exp_mode=modes[mode], descale=inp.descale,
+                        stream=stream, out=out, lse=lse)
+
+    for mode in want:
+        for _ in range(args.warmup):
+            call(mode)
+    torch.cuda.synchronize()
+
+    # alternating rounds; every round times a window of each mode with HIP
+    # events on the stream the kernels run on
+    per_round = max(1, args.steps // args.rounds)
+    windows = {m: [] for m in want}
+    counts = {m: 0 for m in want}
+    for r in range(args.rounds):
+        order = want if r % 2 == 0 else list(reversed(want))
+        for mode in order:
+            n = per_round if r < args.rounds - 1 else args.steps - per_round * (args.rounds - 1)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(n):
+                call(mode)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            windows[mode].append((e0.elapsed_time(e1), n))
+            counts[mode] += n
+
+    def ms_per_call(mode):
+        tot = sum(t for t, _ in windows[mode])
+        return tot / counts[mode]
+
+    flops = w.flops()
+    res_ms = {m: ms_per_call(m) for m in want}
+    tflops = {m: flops / (res_ms[m] * 1e-3) / 1e12 for m in want}
+    head = "h15" if "h15" in want else want[0]
+    peak = PEAK[dtname]
+    achieved = tflops[head]
+    line = {
+        "metric": "attn fwd ms/call + TFLOP/s (% MFMA peak), H15 vs exact-exp speedup @8K",
+        "value": round(achieved, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(res_ms[head], 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dtname,
+        "data": "synthetic (seeded Gaussian Q/K/V, 2% sharp keys where named)",
+        "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "S": w.S, "d": w.d,
+                   "causal": w.causal, "exp_mode": head, "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": None},
+    }
+    if "h15" in want and "exact" in want:
+        med = {m: float(np.median([t / n for t, n in windows[m]])) for m in want}
+        line["control"] = {
+            "exact_ms_per_call": round(res_ms["exact"], 5),
+            "exact_tflops": round(tflops["exact"], 2),
+            "exact_mfma_frac": round(tflops["exact"] / peak, 4),
+            "h15_vs_exact_speedup_pct": round(100.0 * (med["exact"] / med["h15"] - 1.0), 2),
+            "windows_ms_per_call": {m: [round(t / n, 5) for t, n in windows[m]] for m in want},
+        }
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_baseline(w, inp, scale, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

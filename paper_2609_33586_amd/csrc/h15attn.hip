@@ -2,22 +2,22 @@
 // either the hardware exp2 (control) or Rowmax-H15 (Sec. 5.2 Eq. (m-h15),
 // App. B.1 "Implementation"), behind the C ABI declared in h15attn.h.
 //
-// Kernel structure (one workgroup = 8 wave64s = 256 query rows of one head):
+// Kernel structure (one workgroup = 8 wave64s = 256 query rows of one head,
+// two waves per SIMD):
 //   * each wave keeps its 32 query rows of Q in VGPRs as the MFMA B operand;
-//   * key tiles of 128 keys are staged HBM -> VGPR -> LDS, double-buffered:
-//     the loads of tile t+1 are in flight while tile t is computed, and one
-//     barrier per tile separates the buffers;
+//   * key tiles of 128 keys are copied HBM -> LDS with global_load_lds
+//     (no staging registers), double-buffered: the copy of tile t+1 is in
+//     flight while tile t is computed, one barrier per tile;
 //   * scores are computed transposed, S^T = K Q^T, with 32x32 MFMAs (bf16
-//     32x32x16, fp8 32x32x64): each lane then owns one query row and 64 of
-//     the tile's 128 keys, so the row max and row sum are in-lane reductions
-//     plus one exchange with lane ^ 32;
-//   * the weights w are produced in VALU registers (hardware exp2, or the
-//     H15 add/shift), converted to the MFMA operand type and used directly
-//     as the B operand of O^T += V^T P^T: the MFMA contraction index is
-//     mapped to keys so that the S accumulator layout is already the P
-//     operand layout, with V read through the matching key order;
-//   * V is read from LDS with ds_read_b64_tr_b16 (bf16) or stored transposed
-//     in LDS at staging time (fp8).
+//     32x32x16, fp8 32x32x64): each lane owns one query row and 64 of the
+//     tile's 128 keys, so the row max and row sum are in-lane reductions plus
+//     one exchange with lane ^ 32;
+//   * the weights are produced in VALU registers (hardware exp2, or the H15
+//     add/shift), converted to the MFMA operand type and used directly as the
+//     B operand of O^T += V^T P^T: the MFMA contraction index is mapped to
+//     keys so that the S accumulator layout already is the P operand layout;
+//   * V is read from LDS with the transposing reads ds_read_b64_tr_b16 (bf16)
+//     and ds_read_b64_tr_b8 (fp8), in the matching key order.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -27,11 +27,14 @@
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4v __attribute__((__vector_size__(4 * sizeof(__bf16))));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef int i32x8 __attribute__((ext_vector_type(8)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x2v __attribute__((__vector_size__(2 * sizeof(int))));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x4v __attribute__((__vector_size__(4 * sizeof(__bf16))));
+
+#define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
 
 constexpr int NW = 8;           // waves per workgroup
 constexpr int WROWS = 32;       // query rows per wave
@@ -40,9 +43,13 @@ constexpr int BC = 128;         // keys per tile (the running max moves once per
 constexpr int NTHREADS = NW * 64;
 constexpr float H15_MAGIC = 12582912.0f;  // 0x4B400000 = 2^23 + 2^22
 constexpr uint32_t ONE_BITS = 0x3F800000u;
+// clamp at -252 done on the integer form: bits(y + magic) - (0x4B400000 - 252),
+// saturated at zero, is n + 252 clamped at 0 whenever y + magic >= 0
+constexpr uint32_t CLAMP_BASE = 0x4B400000u - 252u;
+constexpr uint32_t CLAMP_BIAS = 0x00800000u;  // bits(2^-126) = bits(1.0) - (252 << 22)
 
 enum { DT_BF16 = 0, DT_FP8 = 1 };
-enum { MODE_EXACT = 0, MODE_H15 = 1 };
+enum { MODE_EXACT = 0, MODE_H15 = 1, MODE_H15_FASTCLAMP = 2 };
 
 struct Params {
   const uint8_t* q;
@@ -66,34 +73,27 @@ struct Cfg {
   static constexpr int EB = DT == DT_BF16 ? 2 : 1;  // operand bytes
   static constexpr int RB = D * EB;                 // bytes per K/V row
   static constexpr int NCH = RB / 16;               // 16-byte chunks per row
-  static constexpr int KT = BC * RB;                // K tile bytes
-  static constexpr int VPITCH = BC + 16;            // fp8: bytes per V^T row (one d)
-  static constexpr int VT = DT == DT_BF16 ? BC * RB : D * VPITCH;
-  static constexpr int BUF = KT + VT;
-  static constexpr int KCH = BC * NCH / NTHREADS;   // K chunks staged per thread
-  static constexpr int VCH = DT == DT_BF16 ? KCH : 1;
-  static constexpr int VSW = NCH >= 16 ? 4 : 2;     // bf16 V swizzle step
-  static_assert(KCH >= 1, "tile too small for the staging layout");
+  static constexpr int TILE = BC * RB;              // bytes of one K (or V) tile
+  static constexpr int BUF = 2 * TILE;              // K then V
+  static constexpr int CHUNKS = BC * NCH;           // 16-byte chunks per tile
+  static constexpr int WAVE_LOADS = CHUNKS / (NW * 64);  // global_load_lds per wave per tile
+  static_assert(WAVE_LOADS >= 1 && CHUNKS % (NW * 64) == 0, "tile/staging mismatch");
 };
 
-// XOR swizzles of 16-byte chunks inside a row (bank spreading for the MFMA
-// operand reads; the staging writes use the same map).
+// Bank-spreading XOR swizzles of the 16-byte chunks of a row.  K rows are read
+// as the MFMA A operand (one chunk of 32 consecutive rows per instruction);
+// V rows through the transposing reads (4 rows x 2 chunks for bf16, 8 rows x
+// 1 chunk for fp8 per 16 lanes).
 template <int DT, int D>
-__device__ __forceinline__ int k_off(int row, int chunk) {
+__device__ __forceinline__ int k_swz(int row) {
   using C = Cfg<DT, D>;
-  return row * C::RB + ((chunk ^ (row % C::NCH)) << 4);
+  return row % C::NCH;
 }
 template <int DT, int D>
-__device__ __forceinline__ int v_off(int row, int byte_in_row) {  // bf16 V, row-major
+__device__ __forceinline__ int v_swz(int row) {
   using C = Cfg<DT, D>;
-  const int chunk = byte_in_row >> 4;
-  return row * C::RB + (((chunk ^ (C::VSW * (row & 3))) % C::NCH) << 4) + (byte_in_row & 15);
-}
-// fp8 V^T position of a key inside the tile: key = 32 blk + 8 m + 4 g + c is
-// stored at 32 blk + 16 g + 4 m + c, so that the 16 keys one MFMA lane half
-// multiplies are contiguous.
-__device__ __forceinline__ int vt_pos(int key) {
-  return (key & ~31) | ((key & 4) << 2) | ((key & 24) >> 1) | (key & 3);
+  if constexpr (DT == DT_BF16) return ((C::NCH >= 16 ? 4 : 2) * (row & 3)) % C::NCH;
+  else return ((row & 3) | (((row >> 3) & 1) << 2)) % C::NCH;
 }
 
 __device__ __forceinline__ void map_block(const Params& p, int L, int& qb, int& b, int& h) {
@@ -118,13 +118,23 @@ __device__ __forceinline__ void map_block(const Params& p, int L, int& qb, int& 
   }
 }
 
+// Rowmax-H15 weight of one score (App. B.1): doubled exponent y, clamp at
+// -252, RNE add of 0x4B400000, left shift by 22, plus the bits of 1.0.
+template <int MODE>
 __device__ __forceinline__ float h15_weight(float s, float c2, float nb2) {
-  // App. B.1: doubled exponent, clamp at -252, RNE add of 0x4B400000, shift
-  // left by 22, add the bits of 1.0 (all modulo 2^32).
-  float y = __builtin_fmaf(s, c2, nb2);
-  y = __builtin_fmaxf(y, -252.0f);
-  const float t = y + H15_MAGIC;
-  return __uint_as_float((__float_as_uint(t) << 22) + ONE_BITS);
+  const float y = __builtin_fmaf(s, c2, nb2);
+  if constexpr (MODE == MODE_H15_FASTCLAMP) {
+    // Same bits as the canonical order when y + magic >= 0 (the launcher only
+    // selects this form when every |y| is provably below 2^22): the clamp
+    // max(n, -252) is taken on n + 252 = bits(t) - CLAMP_BASE with unsigned
+    // saturation, and the bias of the final add absorbs the 252.
+    const float t = y + H15_MAGIC;
+    const uint32_t n252 = __builtin_elementwise_sub_sat(__float_as_uint(t), CLAMP_BASE);
+    return __uint_as_float((n252 << 22) + CLAMP_BIAS);
+  } else {
+    const float t = __builtin_fmaxf(y, -252.0f) + H15_MAGIC;
+    return __uint_as_float((__float_as_uint(t) << 22) + ONE_BITS);
+  }
 }
 
 template <int DT, int D, bool CAUSAL, int MODE, bool PROBE>
@@ -137,6 +147,7 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
   const int wave = tid >> 6;
   const int i32 = lane & 31;
   const int g = lane >> 5;
+  const int G4 = lane >> 4, L16 = lane & 15;
 
   int qb, b, h;
   map_block(p, blockIdx.x, qb, b, h);
@@ -157,86 +168,34 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
 
   // ---- Q block in registers (MFMA B operand: lane holds row i32, k-half g)
   constexpr int NKQ = DT == DT_BF16 ? D / 16 : D / 64;
-  const int qload = min(qrow, S - 1);
-  const uint8_t* qptr = p.q + (q_head + qload) * C::RB;
+  const uint8_t* qptr = p.q + (q_head + min(qrow, S - 1)) * C::RB;
   bf16x8 qb16[DT == DT_BF16 ? NKQ : 1];
   i32x8 qf8[DT == DT_FP8 ? NKQ : 1];
   if constexpr (DT == DT_BF16) {
 #pragma unroll
-    for (int kk = 0; kk < NKQ; ++kk)
-      qb16[kk] = *(const bf16x8*)(qptr + (16 * kk + 8 * g) * 2);
+    for (int kk = 0; kk < NKQ; ++kk) qb16[kk] = *(const bf16x8*)(qptr + (16 * kk + 8 * g) * 2);
   } else {
 #pragma unroll
-    for (int kk = 0; kk < NKQ; ++kk) {
-      const u32x4 lo = *(const u32x4*)(qptr + 64 * kk + 32 * g);
-      const u32x4 hi = *(const u32x4*)(qptr + 64 * kk + 32 * g + 16);
-      qf8[kk] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
-                      (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
-    }
+    for (int kk = 0; kk < NKQ; ++kk) qf8[kk] = *(const i32x8*)(qptr + 64 * kk + 32 * g);
   }
 
-  // ---- staging of one key tile: global -> registers -> LDS
-  u32x4 kreg[C::KCH];
-  u32x4 vreg[DT == DT_BF16 ? C::VCH : 1];
-  u32x2 vreg8[DT == DT_FP8 ? 4 : 1];
-  auto load_tile = [&](int t) {
+  // ---- staging: every wave copies WAVE_LOADS x 1 KB of the K tile and of the
+  // V tile straight into LDS.  LDS slot s (16 bytes) of a tile holds row
+  // s / NCH, chunk (s % NCH) ^ swizzle(row).
+  auto stage_tile = [&](int t, int buf) {
     const int key0 = t * BC;
-#pragma unroll
-    for (int c = 0; c < C::KCH; ++c) {
-      const int cid = tid + c * NTHREADS;
-      const int row = cid / C::NCH, ch = cid % C::NCH;
-      const int key = min(key0 + row, S - 1);
-      kreg[c] = *(const u32x4*)(kg + (size_t)key * C::RB + ch * 16);
-      if constexpr (DT == DT_BF16) vreg[c] = *(const u32x4*)(vg + (size_t)key * C::RB + ch * 16);
-    }
-    if constexpr (DT == DT_FP8) {
-      // item (key group of 4, 8-column chunk); D/8 chunks per key row
-      constexpr int NDC = D / 8;
-      if (tid < (BC / 4) * NDC) {
-        const int kgp = tid / NDC, dc = tid % NDC;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int key = min(key0 + 4 * kgp + e, S - 1);
-          vreg8[e] = *(const u32x2*)(vg + (size_t)key * C::RB + dc * 8);
-        }
-      }
-    }
-  };
-  auto store_tile = [&](int buf) {
     uint8_t* kl = smem + buf * C::BUF;
-    uint8_t* vl = kl + C::KT;
+    uint8_t* vl = kl + C::TILE;
 #pragma unroll
-    for (int c = 0; c < C::KCH; ++c) {
-      const int cid = tid + c * NTHREADS;
-      const int row = cid / C::NCH, ch = cid % C::NCH;
-      *(u32x4*)(kl + k_off<DT, D>(row, ch)) = kreg[c];
-      if constexpr (DT == DT_BF16) *(u32x4*)(vl + v_off<DT, D>(row, ch * 16)) = vreg[c];
-    }
-    if constexpr (DT == DT_FP8) {
-      constexpr int NDC = D / 8;
-      if (tid < (BC / 4) * NDC) {
-        const int kgp = tid / NDC, dc = tid % NDC;
-        const int pos = vt_pos(4 * kgp);
-        // 4 keys x 8 columns of bytes -> 8 columns x 4 keys (byte transpose)
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-          const uint32_t x0 = vreg8[0][half], x1 = vreg8[1][half];
-          const uint32_t x2 = vreg8[2][half], x3 = vreg8[3][half];
-          const uint32_t a_lo = __builtin_amdgcn_perm(x1, x0, 0x05010400u);
-          const uint32_t a_hi = __builtin_amdgcn_perm(x1, x0, 0x07030602u);
-          const uint32_t b_lo = __builtin_amdgcn_perm(x3, x2, 0x05010400u);
-          const uint32_t b_hi = __builtin_amdgcn_perm(x3, x2, 0x07030602u);
-          const uint32_t col[4] = {__builtin_amdgcn_perm(b_lo, a_lo, 0x05040100u),
-                                   __builtin_amdgcn_perm(b_lo, a_lo, 0x07060302u),
-                                   __builtin_amdgcn_perm(b_hi, a_hi, 0x05040100u),
-                                   __builtin_amdgcn_perm(b_hi, a_hi, 0x07060302u)};
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int d = dc * 8 + half * 4 + e;
-            *(uint32_t*)(vl + d * C::VPITCH + pos) = col[e];
-          }
-        }
-      }
+    for (int c = 0; c < C::WAVE_LOADS; ++c) {
+      const int blk = c * NW + wave;  // 1 KB block of the tile
+      const int slot = blk * 64 + lane;
+      const int row = slot / C::NCH, pch = slot % C::NCH;
+      const int key = min(key0 + row, S - 1);
+      const uint8_t* ksrc = kg + (size_t)key * C::RB + ((pch ^ k_swz<DT, D>(row)) << 4);
+      const uint8_t* vsrc = vg + (size_t)key * C::RB + ((pch ^ v_swz<DT, D>(row)) << 4);
+      __builtin_amdgcn_global_load_lds(ksrc, LDS_PTR(void, kl + blk * 1024), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(vsrc, LDS_PTR(void, vl + blk * 1024), 16, 0, 0);
     }
   };
 
@@ -248,55 +207,55 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
   float m_run = -INFINITY;
   float l_part = 0.0f;  // this lane's share of the row sum
 
-  load_tile(0);
-  store_tile(0);
+  stage_tile(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
   for (int t = 0; t < ntiles; ++t) {
     const int buf = t & 1;
-    if (t + 1 < ntiles) load_tile(t + 1);
+    if (t + 1 < ntiles) stage_tile(t + 1, buf ^ 1);
     const int kt0 = t * BC;
     const bool active = wave_live && (!CAUSAL || kt0 <= qw0 + WROWS - 1);
     if (active) {
       const uint8_t* kl = smem + buf * C::BUF;
-      const uint8_t* vl = kl + C::KT;
+      const uint8_t* vl = kl + C::TILE;
 
       // ---- S^T = K Q^T for the 128 keys of the tile (4 blocks of 32 keys)
       f32x16 sacc[4];
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb) sacc[kb] = f32x16{0.0f};
-      const int krow = i32;
+      const int krow_off = i32 * C::RB;
+      const int kswz = k_swz<DT, D>(i32);  // == k_swz(kb * 32 + i32)
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int kk = 0; kk < NKQ; ++kk) {
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb) {
-          const int row = kb * 32 + krow;
+          const uint8_t* rowp = kl + kb * 32 * C::RB + krow_off;
           if constexpr (DT == DT_BF16) {
-            const bf16x8 a = *(const bf16x8*)(kl + k_off<DT, D>(row, 2 * kk + g));
+            const bf16x8 a = *(const bf16x8*)(rowp + (((2 * kk + g) ^ kswz) << 4));
             sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qb16[kk], sacc[kb], 0, 0, 0);
           } else {
-            const u32x4 lo = *(const u32x4*)(kl + k_off<DT, D>(row, 4 * kk + 2 * g));
-            const u32x4 hi = *(const u32x4*)(kl + k_off<DT, D>(row, 4 * kk + 2 * g + 1));
-            const i32x8 a = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
-                                  (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+            const i32x4 lo = *(const i32x4*)(rowp + (((4 * kk + 2 * g) ^ kswz) << 4));
+            const i32x4 hi = *(const i32x4*)(rowp + (((4 * kk + 2 * g + 1) ^ kswz) << 4));
+            const i32x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
             sacc[kb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, qf8[kk], sacc[kb], 0, 0,
                                                                        0, 0, 0, 0);
           }
         }
       }
+      __builtin_amdgcn_s_setprio(0);
       // accumulator value j of block kb holds key kt0 + 32 kb + 8 (j/4) + 4 g + j%4
 
       // ---- masking: causal diagonal and the ragged tail only
       const bool need_mask = (CAUSAL && kt0 + BC - 1 > qw0) || (kt0 + BC > S);
       if (need_mask) {
+        const int lim = (CAUSAL ? min(qrow, S - 1) : S - 1) - kt0 - 4 * g;
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            const int key = kt0 + kb * 32 + 8 * (j >> 2) + 4 * g + (j & 3);
-            const bool bad = (CAUSAL && key > qrow) || key >= S;
-            if (bad) sacc[kb][j] = -INFINITY;
-          }
+          for (int j = 0; j < 16; ++j)
+            if (kb * 32 + 8 * (j >> 2) + (j & 3) > lim) sacc[kb][j] = -INFINITY;
       }
 
       const bool probe_row = PROBE && b == p.pb && h == p.ph && qrow >= p.prow0 &&
@@ -327,14 +286,14 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
 
       // ---- weights, in place over the scores
       float tsum = 0.0f;
-      if constexpr (MODE == MODE_H15) {
+      if constexpr (MODE != MODE_EXACT) {
         const float nb2 = __builtin_fmaf(-m_new, p.c2, 2.0f * off);
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
           for (int j = 0; j < 16; ++j) {
             const float s = sacc[kb][j];
-            float w = h15_weight(s, p.c2, nb2);
+            float w = h15_weight<MODE>(s, p.c2, nb2);
             if (need_mask && s == -INFINITY) w = 0.0f;
             sacc[kb][j] = w;
             tsum += w;
@@ -351,10 +310,13 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
           }
       }
       l_part = l_part * alpha + tsum;
+      // skipping the rescale is exact when no row of the wave moved its max
+      if (__builtin_amdgcn_ballot_w64(alpha != 1.0f) != 0) {
 #pragma unroll
-      for (int db = 0; db < NDB; ++db)
+        for (int db = 0; db < NDB; ++db)
 #pragma unroll
-        for (int j = 0; j < 16; ++j) oacc[db][j] *= alpha;
+          for (int j = 0; j < 16; ++j) oacc[db][j] *= alpha;
+      }
 
       // ---- P in the operand type, then O^T += V^T P^T
       if constexpr (DT == DT_BF16) {
@@ -379,23 +341,28 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
               }
           }
         }
+        // V^T operand: lane (d = i32 + 32 db, half g) needs keys
+        // 16 ks + 8 (r/4) + 4 g + r%4 (r = 0..7): two 4-key transposing reads;
+        // lane L16 of a 16-lane group addresses row 4 g + L16/4 (+8), columns
+        // 16 (G4%2) + 4 (L16%4) .. +3 of the 32-column block.
+        const int vrow = 4 * (G4 >> 1) + (L16 >> 2);
+        const int vcolb = (16 * (G4 & 1) + 4 * (L16 & 3)) * 2;
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
 #pragma unroll
           for (int ks = 0; ks < 8; ++ks) {
-            // keys of this 16-key step: base + 8 (r/4) + 4 g + r%4, r = 0..7
-            const int base = 16 * ks;
-            const int G4 = lane >> 4, L = lane & 15;
-            const int key_a = base + 4 * (G4 >> 1) + (L >> 2);
-            const int col = 32 * db + 16 * (G4 & 1) + 4 * (L & 3);
-            const bf16x4v lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-                (__attribute__((address_space(3))) bf16x4v*)(vl + v_off<DT, D>(key_a, col * 2)));
-            const bf16x4v hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-                (__attribute__((address_space(3))) bf16x4v*)(vl + v_off<DT, D>(key_a + 8, col * 2)));
+            const int r0 = 16 * ks + vrow, r1 = r0 + 8;
+            const int cb = 64 * db + vcolb;
+            const uint8_t* a0 = vl + r0 * C::RB + (((cb >> 4) ^ v_swz<DT, D>(r0)) << 4) + (cb & 15);
+            const uint8_t* a1 = vl + r1 * C::RB + (((cb >> 4) ^ v_swz<DT, D>(r1)) << 4) + (cb & 15);
+            const bf16x4v lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(LDS_PTR(bf16x4v, a0));
+            const bf16x4v hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(LDS_PTR(bf16x4v, a1));
             const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
             oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[ks], oacc[db], 0, 0, 0);
           }
         }
+        __builtin_amdgcn_s_setprio(0);
       } else {
         i32x8 pf[2];
 #pragma unroll
@@ -403,7 +370,8 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
 #pragma unroll
           for (int w4 = 0; w4 < 8; ++w4) {
             const int kb = 2 * t2 + (w4 >> 2), j0 = 4 * (w4 & 3);
-            uint32_t word = 0;
+            // the old value is fully overwritten by the two halves
+            uint32_t word = __float_as_uint(sacc[kb][j0]);
             word = __builtin_amdgcn_cvt_pk_fp8_f32(sacc[kb][j0], sacc[kb][j0 + 1], word, false);
             word = __builtin_amdgcn_cvt_pk_fp8_f32(sacc[kb][j0 + 2], sacc[kb][j0 + 3], word, true);
             pf[t2][w4] = (int)word;
@@ -424,22 +392,36 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
               }
           }
         }
+        // V^T operand: lane (d = i32 + 32 db, half g) needs, for byte r = 8 rd + e,
+        // key 32 (2 t2 + rd/2) + 16 (rd%2) + 8 (e/4) + 4 g + e%4: four 8-key
+        // transposing reads; lane L16 of a 16-lane group addresses row
+        // base + 8 (L16/8) + (L16/2)%4, columns d0 + 8 (L16%2) .. +7.
+        const int vrow = 4 * (G4 >> 1) + 8 * (L16 >> 3) + ((L16 >> 1) & 3);
+        const int vcol = 16 * (G4 & 1) + 8 * (L16 & 1);
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
-          const int d = 32 * db + i32;
 #pragma unroll
           for (int t2 = 0; t2 < 2; ++t2) {
-            const u32x4 lo = *(const u32x4*)(vl + d * C::VPITCH + (2 * t2) * 32 + 16 * g);
-            const u32x4 hi = *(const u32x4*)(vl + d * C::VPITCH + (2 * t2 + 1) * 32 + 16 * g);
-            const i32x8 a = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
-                                  (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+            i32x2v part[4];
+#pragma unroll
+            for (int rd = 0; rd < 4; ++rd) {
+              const int row = 32 * (2 * t2 + (rd >> 1)) + 16 * (rd & 1) + vrow;
+              const int cb = 32 * db + vcol;
+              const uint8_t* a = vl + row * C::RB + (((cb >> 4) ^ v_swz<DT, D>(row)) << 4) + (cb & 15);
+              part[rd] = __builtin_amdgcn_ds_read_tr8_b64_v2i32(LDS_PTR(i32x2v, a));
+            }
+            const i32x4 lo = __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3);
+            const i32x4 hi = __builtin_shufflevector(part[2], part[3], 0, 1, 2, 3);
+            const i32x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
             oacc[db] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, pf[t2], oacc[db], 0, 0,
                                                                        0, 0, 0, 0);
           }
         }
+        __builtin_amdgcn_s_setprio(0);
       }
     }
-    if (t + 1 < ntiles) store_tile(buf ^ 1);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
   }
 
@@ -454,15 +436,14 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
 #pragma unroll
     for (int jq = 0; jq < 4; ++jq) {
       const int col = 32 * db + 8 * jq + 4 * g;
-      uint32_t w01, w23;
-      {
-        const __bf16 a0 = (__bf16)(oacc[db][4 * jq + 0] * inv);
-        const __bf16 a1 = (__bf16)(oacc[db][4 * jq + 1] * inv);
-        const __bf16 a2 = (__bf16)(oacc[db][4 * jq + 2] * inv);
-        const __bf16 a3 = (__bf16)(oacc[db][4 * jq + 3] * inv);
-        w01 = (uint32_t)__builtin_bit_cast(uint16_t, a0) | ((uint32_t)__builtin_bit_cast(uint16_t, a1) << 16);
-        w23 = (uint32_t)__builtin_bit_cast(uint16_t, a2) | ((uint32_t)__builtin_bit_cast(uint16_t, a3) << 16);
-      }
+      const __bf16 a0 = (__bf16)(oacc[db][4 * jq + 0] * inv);
+      const __bf16 a1 = (__bf16)(oacc[db][4 * jq + 1] * inv);
+      const __bf16 a2 = (__bf16)(oacc[db][4 * jq + 2] * inv);
+      const __bf16 a3 = (__bf16)(oacc[db][4 * jq + 3] * inv);
+      const uint32_t w01 = (uint32_t)__builtin_bit_cast(uint16_t, a0) |
+                           ((uint32_t)__builtin_bit_cast(uint16_t, a1) << 16);
+      const uint32_t w23 = (uint32_t)__builtin_bit_cast(uint16_t, a2) |
+                           ((uint32_t)__builtin_bit_cast(uint16_t, a3) << 16);
       *(u32x2*)(orow + col) = u32x2{w01, w23};
     }
   if (p.lse && g == 0)
@@ -490,11 +471,17 @@ hipError_t launch_one(const Params& p, hipStream_t st) {
 template <int DT, int D, bool PROBE>
 hipError_t launch_dt_d(const Params& p, int causal, int mode, hipStream_t st) {
   if (causal) {
-    return mode == ATTN_EXP_H15 ? launch_one<DT, D, true, MODE_H15, PROBE>(p, st)
-                                : launch_one<DT, D, true, MODE_EXACT, PROBE>(p, st);
+    switch (mode) {
+      case MODE_H15: return launch_one<DT, D, true, MODE_H15, PROBE>(p, st);
+      case MODE_H15_FASTCLAMP: return launch_one<DT, D, true, MODE_H15_FASTCLAMP, PROBE>(p, st);
+      default: return launch_one<DT, D, true, MODE_EXACT, PROBE>(p, st);
+    }
   }
-  return mode == ATTN_EXP_H15 ? launch_one<DT, D, false, MODE_H15, PROBE>(p, st)
-                              : launch_one<DT, D, false, MODE_EXACT, PROBE>(p, st);
+  switch (mode) {
+    case MODE_H15: return launch_one<DT, D, false, MODE_H15, PROBE>(p, st);
+    case MODE_H15_FASTCLAMP: return launch_one<DT, D, false, MODE_H15_FASTCLAMP, PROBE>(p, st);
+    default: return launch_one<DT, D, false, MODE_EXACT, PROBE>(p, st);
+  }
 }
 
 template <bool PROBE>
@@ -508,10 +495,22 @@ hipError_t launch_any(const Params& p, int dtype, int d, int causal, int mode, h
 
 bool finite_pos(float x) { return x > 0.0f && x < INFINITY; }
 
+// Kernel variant for an ABI exp_mode.  For FP8 every raw logit satisfies
+// |s| <= d * 448^2, so |y| <= 2 c2 d 448^2 + 16; when that is below 2^22 the
+// H15 exponent y + 0x1.8p23 can never go negative and the integer form of the
+// -252 clamp gives exactly the canonical bits.
+int kernel_mode(int dtype, int exp_mode, int d, float c2) {
+  if (exp_mode == ATTN_EXP_EXACT) return MODE_EXACT;
+  if (dtype == ATTN_FP8_E4M3) {
+    const double ymax = 2.0 * (double)c2 * (double)d * 448.0 * 448.0 * (1.0 + 1e-5) + 16.0;
+    if (ymax < 4194304.0) return MODE_H15_FASTCLAMP;
+  }
+  return MODE_H15;
+}
+
 int fill_params(Params& p, const void* q, const void* k, const void* v, void* o, float* lse, int B,
-                int Hq, int Hkv, int S, int d, int causal, float scale, int dtype, int exp_mode,
+                int Hq, int Hkv, int S, int d, float scale, int dtype, int exp_mode,
                 const attn_opts* opts) {
-  (void)causal;
   if (!q || !k || !v || !o) return ATTN_EINVAL;
   if (B <= 0 || Hq <= 0 || Hkv <= 0 || S <= 0 || d <= 0) return ATTN_EINVAL;
   if (Hq % Hkv != 0) return ATTN_EINVAL;
@@ -573,10 +572,11 @@ int attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse
                 int Hkv, int S, int d, int causal, float scale, int dtype, int exp_mode,
                 const attn_opts* opts) {
   Params p;
-  const int rc = fill_params(p, q, k, v, o, lse, B, Hq, Hkv, S, d, causal, scale, dtype, exp_mode, opts);
+  const int rc = fill_params(p, q, k, v, o, lse, B, Hq, Hkv, S, d, scale, dtype, exp_mode, opts);
   if (rc != ATTN_OK) return rc;
   hipStream_t st = opts ? (hipStream_t)opts->stream : nullptr;
-  const hipError_t e = launch_any<false>(p, dtype, d, causal ? 1 : 0, exp_mode, st);
+  const int mode = kernel_mode(dtype, exp_mode, d, p.c2);
+  const hipError_t e = launch_any<false>(p, dtype, d, causal ? 1 : 0, mode, st);
   return e == hipSuccess ? ATTN_OK : ATTN_ELAUNCH;
 }
 
@@ -590,7 +590,7 @@ int attn_fwd_probe(const void* q, const void* k, const void* v, void* o, float* 
                    const attn_opts* opts, int b, int h, int row0, int nrows, float* s_out,
                    float* w_out, uint32_t* p_bits_out) {
   Params p;
-  const int rc = fill_params(p, q, k, v, o, lse, B, Hq, Hkv, S, d, causal, scale, dtype, exp_mode, opts);
+  const int rc = fill_params(p, q, k, v, o, lse, B, Hq, Hkv, S, d, scale, dtype, exp_mode, opts);
   if (rc != ATTN_OK) return rc;
   if (!s_out || !w_out || !p_bits_out) return ATTN_EINVAL;
   if (b < 0 || b >= B || h < 0 || h >= Hq || row0 < 0 || nrows < 1 || row0 + nrows > S)
@@ -607,8 +607,8 @@ int attn_fwd_probe(const void* q, const void* k, const void* v, void* o, float* 
   hipLaunchKernelGGL(probe_fill, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, s_out, w_out,
                      p_bits_out, n);
   if (hipGetLastError() != hipSuccess) return ATTN_ELAUNCH;
-  hipError_t e;
-  e = launch_any<true>(p, dtype, d, causal ? 1 : 0, exp_mode, st);
+  const int mode = kernel_mode(dtype, exp_mode, d, p.c2);
+  const hipError_t e = launch_any<true>(p, dtype, d, causal ? 1 : 0, mode, st);
   return e == hipSuccess ? ATTN_OK : ATTN_ELAUNCH;
 }
 
