@@ -137,6 +137,29 @@ __device__ __forceinline__ float h15_weight(float s, float c2, float nb2) {
   }
 }
 
+// Tree reductions over a lane's 64 scores (short dependency chains).
+__device__ __forceinline__ float tile_max(const f32x16 (&v)[4]) {
+  float m[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i)
+    m[i] = __builtin_fmaxf(__builtin_fmaxf(v[0][i], v[1][i]), __builtin_fmaxf(v[2][i], v[3][i]));
+#pragma unroll
+  for (int w = 8; w >= 1; w >>= 1)
+#pragma unroll
+    for (int i = 0; i < w; ++i) m[i] = __builtin_fmaxf(m[i], m[i + w]);
+  return m[0];
+}
+__device__ __forceinline__ float tile_sum(const f32x16 (&v)[4]) {
+  float a[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) a[i] = (v[0][i] + v[1][i]) + (v[2][i] + v[3][i]);
+#pragma unroll
+  for (int w = 8; w >= 1; w >>= 1)
+#pragma unroll
+    for (int i = 0; i < w; ++i) a[i] = a[i] + a[i + w];
+  return a[0];
+}
+
 template <int DT, int D, bool CAUSAL, int MODE, bool PROBE>
 __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
   using C = Cfg<DT, D>;
@@ -274,11 +297,7 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
       }
 
       // ---- running maximum (threshold 0: moves to the maximum so far)
-      float mt = -INFINITY;
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int j = 0; j < 16; ++j) mt = __builtin_fmaxf(mt, sacc[kb][j]);
+      float mt = tile_max(sacc);
       mt = __builtin_fmaxf(mt, __shfl_xor(mt, 32));
       const float m_new = __builtin_fmaxf(m_run, mt);
       const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * p.c1);
@@ -292,22 +311,32 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
           for (int j = 0; j < 16; ++j) {
-            const float s = sacc[kb][j];
-            float w = h15_weight<MODE>(s, p.c2, nb2);
-            if (need_mask && s == -INFINITY) w = 0.0f;
+            const float w = h15_weight<MODE>(sacc[kb][j], p.c2, nb2);
             sacc[kb][j] = w;
-            tsum += w;
           }
+        if (need_mask) {
+          // masked keys carry weight 0 (the clamp alone would give 2^-126).
+          // The limit is laundered through an empty asm so the compiler does
+          // not share these comparisons with the score masking above, which
+          // would keep 64 masks live across every tile.
+          int lim = (CAUSAL ? min(qrow, S - 1) : S - 1) - kt0 - 4 * g;
+          asm volatile("" : "+v"(lim));
+#pragma unroll
+          for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int j = 0; j < 16; ++j)
+              if (kb * 32 + 8 * (j >> 2) + (j & 3) > lim) sacc[kb][j] = 0.0f;
+        }
+        tsum = tile_sum(sacc);
       } else {
         const float nb1 = __builtin_fmaf(-m_new, p.c1, off);
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
           for (int j = 0; j < 16; ++j) {
-            const float w = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][j], p.c1, nb1));
-            sacc[kb][j] = w;
-            tsum += w;
+            sacc[kb][j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][j], p.c1, nb1));
           }
+        tsum = tile_sum(sacc);
       }
       l_part = l_part * alpha + tsum;
       // skipping the rescale is exact when no row of the wave moved its max
