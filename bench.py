@@ -32,7 +32,7 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=30)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--rounds", type=int, default=3)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
@@ -71,6 +71,23 @@ def cpu_baseline(w, inp, scale, target_s):
     return {"value": flops_done / spent / 1e12, "unit": "TFLOP/s", "cores": oracle.threads(), "kind": "oracle",
             "sample": f"{rows_done} random query rows of the workload (H15 per-tile mode), {spent:.1f} s; "
                       f"FLOPs counted per row as 4*keys*d"}
+
+
+def profiled_traffic(workload: str, mode: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, when it
+    was taken on the kernel source as it is now (else None)."""
+    import hashlib
+    path = ROOT / "profiles" / "hbm_traffic.txt"
+    src = ROOT / "paper_2609_33586_amd" / "csrc" / "h15attn.hip"
+    try:
+        rec = json.loads(path.read_text())
+        sha = hashlib.sha256(src.read_bytes()).hexdigest()[:16]
+        if rec.get("source_sha256_prefix") != sha:
+            return None
+        t = rec["workloads"][workload][mode]
+        return int(t["hbm_read_bytes"] + t["hbm_write_bytes"])
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def main():
@@ -166,7 +183,7 @@ def main():
         "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "S": w.S, "d": w.d,
                    "causal": w.causal, "exp_mode": head, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
-                     "frac": round(achieved / peak, 4), "traffic": None},
+                     "frac": round(achieved / peak, 4), "traffic": profiled_traffic(w.name, head)},
     }
     if "h15" in want and "exact" in want:
         med = {m: float(np.median([t / n for t, n in windows[m]])) for m in want}
