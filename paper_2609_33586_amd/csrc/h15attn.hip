@@ -41,6 +41,14 @@ constexpr int WROWS = 32;       // query rows per wave
 constexpr int BR = NW * WROWS;  // query rows per workgroup
 constexpr int BC = 128;         // keys per tile (the running max moves once per tile)
 constexpr int NTHREADS = NW * 64;
+// LDS operand prefetch distance (in MFMAs) of the QK^T and PV products
+constexpr int QK_AHEAD = 3;
+constexpr int PV_AHEAD = 3;
+// word 3 of a raw buffer resource on CDNA (32-bit data format, no swizzle)
+constexpr int BUF_DWORD3 = 0x00020000;
+// instruction classes of __builtin_amdgcn_sched_group_barrier
+constexpr int SG_MFMA = 0x008;
+constexpr int SG_DS_READ = 0x100;
 constexpr float H15_MAGIC = 12582912.0f;  // 0x4B400000 = 2^23 + 2^22
 constexpr uint32_t ONE_BITS = 0x3F800000u;
 // clamp at -252 done on the integer form: bits(y + magic) - (0x4B400000 - 252),
@@ -137,17 +145,30 @@ __device__ __forceinline__ float h15_weight(float s, float c2, float nb2) {
   }
 }
 
-// Tree reductions over a lane's 64 scores (short dependency chains).
+// Tree reductions over a lane's 64 scores (short dependency chains).  The
+// maximum is taken with v_max3_f32 directly: fmaxf on matrix-core results
+// would first canonicalize every input (one extra instruction per score).
+__device__ __forceinline__ float max3(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
 __device__ __forceinline__ float tile_max(const f32x16 (&v)[4]) {
-  float m[16];
+  // 64 -> 22 -> 8 -> 3 -> 1
+  float a[22], b[8], c[3];
 #pragma unroll
-  for (int i = 0; i < 16; ++i)
-    m[i] = __builtin_fmaxf(__builtin_fmaxf(v[0][i], v[1][i]), __builtin_fmaxf(v[2][i], v[3][i]));
+  for (int i = 0; i < 21; ++i) {
+    const int e0 = 3 * i, e1 = 3 * i + 1, e2 = 3 * i + 2;
+    a[i] = max3(v[e0 >> 4][e0 & 15], v[e1 >> 4][e1 & 15], v[e2 >> 4][e2 & 15]);
+  }
+  a[21] = v[3][15];
 #pragma unroll
-  for (int w = 8; w >= 1; w >>= 1)
-#pragma unroll
-    for (int i = 0; i < w; ++i) m[i] = __builtin_fmaxf(m[i], m[i + w]);
-  return m[0];
+  for (int i = 0; i < 7; ++i) b[i] = max3(a[3 * i], a[3 * i + 1], a[3 * i + 2]);
+  b[7] = a[21];
+  c[0] = max3(b[0], b[1], b[2]);
+  c[1] = max3(b[3], b[4], b[5]);
+  c[2] = max3(b[6], b[7], b[7]);
+  return max3(c[0], c[1], c[2]);
 }
 __device__ __forceinline__ float tile_sum(const f32x16 (&v)[4]) {
   float a[16];
@@ -204,7 +225,11 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
 
   // ---- staging: every wave copies WAVE_LOADS x 1 KB of the K tile and of the
   // V tile straight into LDS.  LDS slot s (16 bytes) of a tile holds row
-  // s / NCH, chunk (s % NCH) ^ swizzle(row).
+  // s / NCH, chunk (s % NCH) ^ swizzle(row).  Buffer (not global) loads are
+  // used so that the compiler's wait counting keeps LDS reads pipelined while
+  // these copies are in flight.  One head's rows span S * RB < 2^31 bytes.
+  const __amdgpu_buffer_rsrc_t krsrc = __builtin_amdgcn_make_buffer_rsrc((void*)kg, (short)0, S * C::RB, BUF_DWORD3);
+  const __amdgpu_buffer_rsrc_t vrsrc = __builtin_amdgcn_make_buffer_rsrc((void*)vg, (short)0, S * C::RB, BUF_DWORD3);
   auto stage_tile = [&](int t, int buf) {
     const int key0 = t * BC;
     uint8_t* kl = smem + buf * C::BUF;
@@ -214,11 +239,11 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
       const int blk = c * NW + wave;  // 1 KB block of the tile
       const int slot = blk * 64 + lane;
       const int row = slot / C::NCH, pch = slot % C::NCH;
-      const int key = min(key0 + row, S - 1);
-      const uint8_t* ksrc = kg + (size_t)key * C::RB + ((pch ^ k_swz<DT, D>(row)) << 4);
-      const uint8_t* vsrc = vg + (size_t)key * C::RB + ((pch ^ v_swz<DT, D>(row)) << 4);
-      __builtin_amdgcn_global_load_lds(ksrc, LDS_PTR(void, kl + blk * 1024), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(vsrc, LDS_PTR(void, vl + blk * 1024), 16, 0, 0);
+      const uint32_t rowoff = (uint32_t)min(key0 + row, S - 1) * C::RB;
+      const uint32_t koff = rowoff + ((pch ^ k_swz<DT, D>(row)) << 4);
+      const uint32_t voff = rowoff + ((pch ^ v_swz<DT, D>(row)) << 4);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(krsrc, LDS_PTR(void, kl + blk * 1024), 16, koff, 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vrsrc, LDS_PTR(void, vl + blk * 1024), 16, voff, 0, 0, 0);
     }
   };
 
@@ -249,22 +274,54 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
       for (int kb = 0; kb < 4; ++kb) sacc[kb] = f32x16{0.0f};
       const int krow_off = i32 * C::RB;
       const int kswz = k_swz<DT, D>(i32);  // == k_swz(kb * 32 + i32)
+      // MFMA i covers (kk = i / 4, kb = i % 4).  Its K operand is read from LDS
+      // QK_AHEAD MFMAs in advance into a ring of registers, and the schedule
+      // below keeps that order, so each MFMA finds its operand loaded.
+      constexpr int NQK = 4 * NKQ;
       __builtin_amdgcn_s_setprio(1);
+      if constexpr (DT == DT_BF16) {
+        auto ldk = [&](int i) {
+          const uint8_t* rowp = kl + (i & 3) * 32 * C::RB + krow_off;
+          return *(const bf16x8*)(rowp + (((2 * (i >> 2) + g) ^ kswz) << 4));
+        };
+        bf16x8 ring[QK_AHEAD + 1];
 #pragma unroll
-      for (int kk = 0; kk < NKQ; ++kk) {
+        for (int i = 0; i < QK_AHEAD; ++i) ring[i] = ldk(i);
+        __builtin_amdgcn_sched_barrier(0);  // the prologue reads go first
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb) {
-          const uint8_t* rowp = kl + kb * 32 * C::RB + krow_off;
-          if constexpr (DT == DT_BF16) {
-            const bf16x8 a = *(const bf16x8*)(rowp + (((2 * kk + g) ^ kswz) << 4));
-            sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qb16[kk], sacc[kb], 0, 0, 0);
-          } else {
-            const i32x4 lo = *(const i32x4*)(rowp + (((4 * kk + 2 * g) ^ kswz) << 4));
-            const i32x4 hi = *(const i32x4*)(rowp + (((4 * kk + 2 * g + 1) ^ kswz) << 4));
-            const i32x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-            sacc[kb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, qf8[kk], sacc[kb], 0, 0,
-                                                                       0, 0, 0, 0);
-          }
+        for (int i = 0; i < NQK; ++i) {
+          const int kk = i >> 2, kb = i & 3;
+          sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ring[i % (QK_AHEAD + 1)], qb16[kk], sacc[kb], 0, 0, 0);
+          if (i + QK_AHEAD < NQK) ring[(i + QK_AHEAD) % (QK_AHEAD + 1)] = ldk(i + QK_AHEAD);
+        }
+#pragma unroll
+        for (int i = 0; i < NQK; ++i) {
+          __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+          if (i + QK_AHEAD < NQK) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
+        }
+      } else {
+        auto ldk = [&](int i) {
+          const int kk = i >> 2;
+          const uint8_t* rowp = kl + (i & 3) * 32 * C::RB + krow_off;
+          const i32x4 lo = *(const i32x4*)(rowp + (((4 * kk + 2 * g) ^ kswz) << 4));
+          const i32x4 hi = *(const i32x4*)(rowp + (((4 * kk + 2 * g + 1) ^ kswz) << 4));
+          return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        };
+        i32x8 ring[QK_AHEAD + 1];
+#pragma unroll
+        for (int i = 0; i < QK_AHEAD; ++i) ring[i] = ldk(i);
+        __builtin_amdgcn_sched_barrier(0);  // the prologue reads go first
+#pragma unroll
+        for (int i = 0; i < NQK; ++i) {
+          const int kk = i >> 2, kb = i & 3;
+          sacc[kb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ring[i % (QK_AHEAD + 1)], qf8[kk], sacc[kb],
+                                                                     0, 0, 0, 0, 0, 0);
+          if (i + QK_AHEAD < NQK) ring[(i + QK_AHEAD) % (QK_AHEAD + 1)] = ldk(i + QK_AHEAD);
+        }
+#pragma unroll
+        for (int i = 0; i < NQK; ++i) {
+          __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+          if (i + QK_AHEAD < NQK) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 2, 0);
         }
       }
       __builtin_amdgcn_s_setprio(0);
@@ -297,9 +354,8 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
       }
 
       // ---- running maximum (threshold 0: moves to the maximum so far)
-      float mt = tile_max(sacc);
-      mt = __builtin_fmaxf(mt, __shfl_xor(mt, 32));
-      const float m_new = __builtin_fmaxf(m_run, mt);
+      const float mt = tile_max(sacc);
+      const float m_new = max3(m_run, mt, __shfl_xor(mt, 32));
       const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * p.c1);
       m_run = m_new;
 
@@ -376,20 +432,31 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
         // 16 (G4%2) + 4 (L16%4) .. +3 of the 32-column block.
         const int vrow = 4 * (G4 >> 1) + (L16 >> 2);
         const int vcolb = (16 * (G4 & 1) + 4 * (L16 & 3)) * 2;
+        // MFMA i covers (db = i / 8, ks = i % 8); V operands run PV_AHEAD ahead
+        auto ldv = [&](int i) {
+          const int r0 = 16 * (i & 7) + vrow, r1 = r0 + 8;
+          const int cb = 64 * (i >> 3) + vcolb;
+          const uint8_t* a0 = vl + r0 * C::RB + (((cb >> 4) ^ v_swz<DT, D>(r0)) << 4) + (cb & 15);
+          const uint8_t* a1 = vl + r1 * C::RB + (((cb >> 4) ^ v_swz<DT, D>(r1)) << 4) + (cb & 15);
+          const bf16x4v lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(LDS_PTR(bf16x4v, a0));
+          const bf16x4v hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(LDS_PTR(bf16x4v, a1));
+          return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        };
+        constexpr int NPV = NDB * 8;
+        bf16x8 ring[PV_AHEAD + 1];
         __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) {
+        for (int i = 0; i < PV_AHEAD; ++i) ring[i] = ldv(i);
+        __builtin_amdgcn_sched_barrier(0);  // the prologue reads go first
 #pragma unroll
-          for (int ks = 0; ks < 8; ++ks) {
-            const int r0 = 16 * ks + vrow, r1 = r0 + 8;
-            const int cb = 64 * db + vcolb;
-            const uint8_t* a0 = vl + r0 * C::RB + (((cb >> 4) ^ v_swz<DT, D>(r0)) << 4) + (cb & 15);
-            const uint8_t* a1 = vl + r1 * C::RB + (((cb >> 4) ^ v_swz<DT, D>(r1)) << 4) + (cb & 15);
-            const bf16x4v lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(LDS_PTR(bf16x4v, a0));
-            const bf16x4v hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(LDS_PTR(bf16x4v, a1));
-            const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-            oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[ks], oacc[db], 0, 0, 0);
-          }
+        for (int i = 0; i < NPV; ++i) {
+          oacc[i >> 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ring[i % (PV_AHEAD + 1)], pb[i & 7], oacc[i >> 3], 0, 0, 0);
+          if (i + PV_AHEAD < NPV) ring[(i + PV_AHEAD) % (PV_AHEAD + 1)] = ldv(i + PV_AHEAD);
+        }
+#pragma unroll
+        for (int i = 0; i < NPV; ++i) {
+          __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 1);
+          if (i + PV_AHEAD < NPV) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 2, 1);
         }
         __builtin_amdgcn_s_setprio(0);
       } else {
@@ -427,25 +494,37 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
         // base + 8 (L16/8) + (L16/2)%4, columns d0 + 8 (L16%2) .. +7.
         const int vrow = 4 * (G4 >> 1) + 8 * (L16 >> 3) + ((L16 >> 1) & 3);
         const int vcol = 16 * (G4 & 1) + 8 * (L16 & 1);
+        // MFMA i covers (db = i / 2, t2 = i % 2); V operands run PV_AHEAD ahead
+        auto ldv = [&](int i) {
+          const int db = i >> 1, t2 = i & 1;
+          i32x2v part[4];
+#pragma unroll
+          for (int rd = 0; rd < 4; ++rd) {
+            const int row = 32 * (2 * t2 + (rd >> 1)) + 16 * (rd & 1) + vrow;
+            const int cb = 32 * db + vcol;
+            const uint8_t* a = vl + row * C::RB + (((cb >> 4) ^ v_swz<DT, D>(row)) << 4) + (cb & 15);
+            part[rd] = __builtin_amdgcn_ds_read_tr8_b64_v2i32(LDS_PTR(i32x2v, a));
+          }
+          const i32x4 lo = __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3);
+          const i32x4 hi = __builtin_shufflevector(part[2], part[3], 0, 1, 2, 3);
+          return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        };
+        constexpr int NPV = NDB * 2;
+        i32x8 ring[PV_AHEAD + 1];
         __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) {
+        for (int i = 0; i < PV_AHEAD; ++i) ring[i] = ldv(i);
+        __builtin_amdgcn_sched_barrier(0);  // the prologue reads go first
 #pragma unroll
-          for (int t2 = 0; t2 < 2; ++t2) {
-            i32x2v part[4];
+        for (int i = 0; i < NPV; ++i) {
+          oacc[i >> 1] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ring[i % (PV_AHEAD + 1)], pf[i & 1],
+                                                                         oacc[i >> 1], 0, 0, 0, 0, 0, 0);
+          if (i + PV_AHEAD < NPV) ring[(i + PV_AHEAD) % (PV_AHEAD + 1)] = ldv(i + PV_AHEAD);
+        }
 #pragma unroll
-            for (int rd = 0; rd < 4; ++rd) {
-              const int row = 32 * (2 * t2 + (rd >> 1)) + 16 * (rd & 1) + vrow;
-              const int cb = 32 * db + vcol;
-              const uint8_t* a = vl + row * C::RB + (((cb >> 4) ^ v_swz<DT, D>(row)) << 4) + (cb & 15);
-              part[rd] = __builtin_amdgcn_ds_read_tr8_b64_v2i32(LDS_PTR(i32x2v, a));
-            }
-            const i32x4 lo = __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3);
-            const i32x4 hi = __builtin_shufflevector(part[2], part[3], 0, 1, 2, 3);
-            const i32x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-            oacc[db] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, pf[t2], oacc[db], 0, 0,
-                                                                       0, 0, 0, 0);
-          }
+        for (int i = 0; i < NPV; ++i) {
+          __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 1);
+          if (i + PV_AHEAD < NPV) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 4, 1);
         }
         __builtin_amdgcn_s_setprio(0);
       }
@@ -560,6 +639,8 @@ int fill_params(Params& p, const void* q, const void* k, const void* v, void* o,
   }
   const long long rows = (long long)B * Hq * S;
   if (rows > (1LL << 31) / 2) return ATTN_EUNSUPPORTED;
+  // one head's K or V rows are addressed with 32-bit byte offsets
+  if ((long long)S * d * (dtype == ATTN_BF16 ? 2 : 1) > INT32_MAX) return ATTN_EUNSUPPORTED;
   p = Params{};
   p.q = (const uint8_t*)q;
   p.k = (const uint8_t*)k;
