@@ -63,7 +63,9 @@ enum attn_status {
     ATTN_EINVAL = -1,      /* null pointer, non-positive size, Hq % Hkv != 0,
                               scale or descale not positive and finite */
     ATTN_EUNSUPPORTED = -2, /* d not in {64, 128}, unknown dtype or exp_mode,
-                              pointer not 16-byte aligned */
+                              pointer not 16-byte aligned, B*Hq*S > 2^30, or
+                              one head's K/V rows (S * d * element bytes)
+                              not addressable with 31-bit offsets */
     ATTN_ELAUNCH = -3      /* the HIP launch reported an error */
 };
 

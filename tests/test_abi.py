@@ -62,6 +62,9 @@ def test_invalid_arguments(L):
     assert call(L, dtype=2) == E_UNS and call(L, mode=5) == E_UNS
     assert call(L, q=FAKE + 8) == E_UNS
     assert call(L, lse=FAKE + 2) == E_UNS
+    # size limits: B*Hq*S rows, and one head's K/V bytes within 31-bit offsets
+    assert call(L, B=4, Hq=2, Hkv=1, S=1 << 27) == E_UNS
+    assert call(L, B=1, Hq=1, Hkv=1, S=1 << 23, d=128, dtype=0) == E_UNS
     # FP8 needs positive finite descales
     assert call(L, dtype=1) == E_INV
     for bad in ((0.0, 1.0, 1.0), (1.0, -1.0, 1.0), (1.0, 1.0, math.inf)):
