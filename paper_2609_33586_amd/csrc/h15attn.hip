@@ -22,6 +22,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "h15attn.h"
 
 namespace {
@@ -33,14 +35,22 @@ typedef int i32x8 __attribute__((ext_vector_type(8)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x2v __attribute__((__vector_size__(2 * sizeof(int))));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 #define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
 
-constexpr int NW = 8;           // waves per workgroup
-constexpr int WROWS = 32;       // query rows per wave
-constexpr int BR = NW * WROWS;  // query rows per workgroup
-constexpr int BC = 128;         // keys per tile (the running max moves once per tile)
-constexpr int NTHREADS = NW * 64;
+enum { DT_BF16 = 0, DT_FP8 = 1 };
+
+constexpr int WROWS = 32;  // query rows per wave
+constexpr int BC = 128;    // keys per tile (the running max moves once per tile)
+// Waves per workgroup: 4 for FP8 (two workgroups share a CU, so one's
+// barrier and prologue stalls overlap the other's work), 8 for BF16 (whose
+// double-buffered tiles leave LDS for only one workgroup per CU).
+template <int DT>
+constexpr int waves_per_group() {
+  return DT == DT_FP8 ? 4 : 8;
+}
+constexpr int MAX_THREADS = 8 * 64;
 // LDS operand prefetch distance (in MFMAs) of the QK^T and PV products
 constexpr int QK_AHEAD = 3;
 constexpr int PV_AHEAD = 3;
@@ -56,7 +66,6 @@ constexpr uint32_t ONE_BITS = 0x3F800000u;
 constexpr uint32_t CLAMP_BASE = 0x4B400000u - 252u;
 constexpr uint32_t CLAMP_BIAS = 0x00800000u;  // bits(2^-126) = bits(1.0) - (252 << 22)
 
-enum { DT_BF16 = 0, DT_FP8 = 1 };
 enum { MODE_EXACT = 0, MODE_H15 = 1, MODE_H15_FASTCLAMP = 2 };
 
 struct Params {
@@ -84,8 +93,9 @@ struct Cfg {
   static constexpr int TILE = BC * RB;              // bytes of one K (or V) tile
   static constexpr int BUF = 2 * TILE;              // K then V
   static constexpr int CHUNKS = BC * NCH;           // 16-byte chunks per tile
-  static constexpr int WAVE_LOADS = CHUNKS / (NW * 64);  // global_load_lds per wave per tile
-  static_assert(WAVE_LOADS >= 1 && CHUNKS % (NW * 64) == 0, "tile/staging mismatch");
+  static constexpr int NW = waves_per_group<DT>();  // waves per workgroup
+  static constexpr int BR = NW * WROWS;             // query rows per workgroup
+  static_assert(CHUNKS % (NW * 64) == 0, "tile/staging mismatch");
 };
 
 // Bank-spreading XOR swizzles of the 16-byte chunks of a row.  K rows are read
@@ -145,6 +155,73 @@ __device__ __forceinline__ float h15_weight(float s, float c2, float nb2) {
   }
 }
 
+// x, or y where key offset C lies beyond this lane's last valid offset lim.
+// Compare and select go through VCC together (C as an immediate): written
+// as plain C the compiler keeps all 64 masks of a tile live in scalar
+// registers at once.
+template <int C>
+__device__ __forceinline__ float select_beyond(int lim, float x, float y) {
+  float r;
+  // volatile: keeps the masking inside the branch that needs it
+  asm volatile("v_cmp_gt_i32 vcc, %1, %2\n\tv_cndmask_b32 %0, %3, %4, vcc"
+               : "=v"(r)
+               : "n"(C), "v"(lim), "v"(x), "v"(y)
+               : "vcc");
+  return r;
+}
+// y over the scores of a tile whose key offset lies beyond lim
+template <int E = 0>
+__device__ __forceinline__ void mask_beyond(f32x16 (&v)[4], int lim, float y) {
+  if constexpr (E < 64) {
+    constexpr int kb = E / 16, j = E % 16;
+    v[kb][j] = select_beyond<kb * 32 + 8 * (j >> 2) + (j & 3)>(lim, v[kb][j], y);
+    mask_beyond<E + 1>(v, lim, y);
+  }
+}
+
+// This lane's value and that of lane i ^ 32 (in an order that depends on the
+// lane), exchanged on the VALU rather than through LDS.
+__device__ __forceinline__ void with_partner(float x, float& a, float& b) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  a = __uint_as_float(r[0]);
+  b = __uint_as_float(r[1]);
+}
+
+// Compile-time loop: f(integral_constant<int, I>) for I in [B, E).
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
+// Transposing LDS reads written as inline asm.  The compiler's wait counting
+// would make the intrinsic forms wait for every LDS copy in flight (it cannot
+// tell that those copies land in other buffers); here the caller waits for
+// the reads itself with lds_wait, which also orders the uses after the wait.
+template <int OFF>
+__device__ __forceinline__ i32x2v ds_read_tr8(uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset");
+  i32x2v r;
+  asm volatile("ds_read_b64_tr_b8 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "n"(OFF));
+  return r;
+}
+template <int OFF>
+__device__ __forceinline__ i32x2v ds_read_tr16(uint32_t addr) {
+  static_assert(OFF >= 0 && OFF < 65536, "ds offset");
+  i32x2v r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "n"(OFF));
+  return r;
+}
+// Wait until at most N LDS operations of this wave are outstanding (they
+// complete in order), then hand x on as produced after the wait.
+template <int N, typename T>
+__device__ __forceinline__ void lds_wait(T& x) {
+  static_assert(N >= 0 && N < 16, "lgkmcnt range");
+  asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(x) : "n"(N));
+}
+
 // Tree reductions over a lane's 64 scores (short dependency chains).  The
 // maximum is taken with v_max3_f32 directly: fmaxf on matrix-core results
 // would first canonicalize every input (one extra instruction per score).
@@ -182,9 +259,12 @@ __device__ __forceinline__ float tile_sum(const f32x16 (&v)[4]) {
 }
 
 template <int DT, int D, bool CAUSAL, int MODE, bool PROBE>
-__global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
+__global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd_kernel(Params p) {
   using C = Cfg<DT, D>;
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * C::BUF];
+  constexpr int NW = C::NW, BR = C::BR;
+  // K and V tiles, each double-buffered
+  constexpr int NSTAGE = 2;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[NSTAGE * C::BUF];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -223,29 +303,44 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
     for (int kk = 0; kk < NKQ; ++kk) qf8[kk] = *(const i32x8*)(qptr + 64 * kk + 32 * g);
   }
 
-  // ---- staging: every wave copies WAVE_LOADS x 1 KB of the K tile and of the
-  // V tile straight into LDS.  LDS slot s (16 bytes) of a tile holds row
-  // s / NCH, chunk (s % NCH) ^ swizzle(row).  Buffer (not global) loads are
-  // used so that the compiler's wait counting keeps LDS reads pipelined while
-  // these copies are in flight.  One head's rows span S * RB < 2^31 bytes.
+  // ---- staging: every wave copies WAVE_LOADS x 1 KB of a K or V tile
+  // straight into LDS.  LDS slot s (16 bytes) of a tile holds row s / NCH,
+  // chunk (s % NCH) ^ swizzle(row).  Buffer (not global) loads are used so
+  // that the compiler's wait counting keeps LDS reads pipelined while these
+  // copies are in flight.  One head's rows span S * RB < 2^31 bytes.  Tile t
+  // uses K buffer t % 2 and V buffer t % 2.
   const __amdgpu_buffer_rsrc_t krsrc = __builtin_amdgcn_make_buffer_rsrc((void*)kg, (short)0, S * C::RB, BUF_DWORD3);
   const __amdgpu_buffer_rsrc_t vrsrc = __builtin_amdgcn_make_buffer_rsrc((void*)vg, (short)0, S * C::RB, BUF_DWORD3);
-  auto stage_tile = [&](int t, int buf) {
-    const int key0 = t * BC;
-    uint8_t* kl = smem + buf * C::BUF;
-    uint8_t* vl = kl + C::TILE;
+  auto kbuf = [&](int t) { return smem + (t & 1) * C::BUF; };
+  auto vbuf = [&](int t) { return smem + (t & 1) * C::BUF + C::TILE; };
+  // waves [W0, W0 + NWS) copy the tile
+  auto stage_k = [&](int t, auto nws, int w0) {
+    constexpr int NWS = decltype(nws)::value;
+    static_assert(C::CHUNKS % (NWS * 64) == 0, "tile/staging mismatch");
+    uint8_t* dst = kbuf(t);
 #pragma unroll
-    for (int c = 0; c < C::WAVE_LOADS; ++c) {
-      const int blk = c * NW + wave;  // 1 KB block of the tile
+    for (int c = 0; c < C::CHUNKS / (NWS * 64); ++c) {
+      const int blk = c * NWS + (wave - w0);  // 1 KB block of the tile
       const int slot = blk * 64 + lane;
       const int row = slot / C::NCH, pch = slot % C::NCH;
-      const uint32_t rowoff = (uint32_t)min(key0 + row, S - 1) * C::RB;
-      const uint32_t koff = rowoff + ((pch ^ k_swz<DT, D>(row)) << 4);
-      const uint32_t voff = rowoff + ((pch ^ v_swz<DT, D>(row)) << 4);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(krsrc, LDS_PTR(void, kl + blk * 1024), 16, koff, 0, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(vrsrc, LDS_PTR(void, vl + blk * 1024), 16, voff, 0, 0, 0);
+      const uint32_t off = (uint32_t)min(t * BC + row, S - 1) * C::RB + ((pch ^ k_swz<DT, D>(row)) << 4);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(krsrc, LDS_PTR(void, dst + blk * 1024), 16, off, 0, 0, 0);
     }
   };
+  auto stage_v = [&](int t, auto nws, int w0) {
+    constexpr int NWS = decltype(nws)::value;
+    static_assert(C::CHUNKS % (NWS * 64) == 0, "tile/staging mismatch");
+    uint8_t* dst = vbuf(t);
+#pragma unroll
+    for (int c = 0; c < C::CHUNKS / (NWS * 64); ++c) {
+      const int blk = c * NWS + (wave - w0);
+      const int slot = blk * 64 + lane;
+      const int row = slot / C::NCH, pch = slot % C::NCH;
+      const uint32_t off = (uint32_t)min(t * BC + row, S - 1) * C::RB + ((pch ^ v_swz<DT, D>(row)) << 4);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vrsrc, LDS_PTR(void, dst + blk * 1024), 16, off, 0, 0, 0);
+    }
+  };
+  constexpr std::integral_constant<int, NW> ALL_WAVES{};
 
   // ---- running state (this lane's query row; lanes i and i^32 agree on m)
   constexpr int NDB = D / 32;  // 32-column blocks of O^T
@@ -254,280 +349,272 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
   for (int db = 0; db < NDB; ++db) oacc[db] = f32x16{0.0f};
   float m_run = -INFINITY;
   float l_part = 0.0f;  // this lane's share of the row sum
+  // scores, then weights, of the current tile; accumulator value j of block
+  // kb holds key 32 kb + 8 (j/4) + 4 g + j%4 of the tile
+  f32x16 sacc[4];
+  // P of the current tile in the operand type (the MFMA B operand of PV)
+  bf16x8 pb[DT == DT_BF16 ? 8 : 1];
+  i32x8 pf[DT == DT_FP8 ? 2 : 1];
 
-  stage_tile(0, 0);
+  // ---- S^T = K Q^T for the 128 keys of a tile (4 blocks of 32 keys).
+  // MFMA i covers (kk = i / 4, kb = i % 4).  Its K operand is read from LDS
+  // QK_AHEAD MFMAs in advance into a ring of registers, and the schedule keeps
+  // that order, so each MFMA finds its operand loaded.
+  auto qk = [&](const uint8_t* kl) {
+    const int krow_off = i32 * C::RB;
+    const int kswz = k_swz<DT, D>(i32);  // == k_swz(kb * 32 + i32)
+    constexpr int NQK = 4 * NKQ;
+    if constexpr (DT == DT_BF16) {
+      auto ldk = [&](int i) {
+        const uint8_t* rowp = kl + (i & 3) * 32 * C::RB + krow_off;
+        return *(const bf16x8*)(rowp + (((2 * (i >> 2) + g) ^ kswz) << 4));
+      };
+      bf16x8 ring[QK_AHEAD + 1];
+#pragma unroll
+      for (int i = 0; i < QK_AHEAD; ++i) ring[i] = ldk(i);
+      __builtin_amdgcn_sched_barrier(0);  // the prologue reads go first
+#pragma unroll
+      for (int i = 0; i < NQK; ++i) {
+        const int kk = i >> 2, kb = i & 3;
+        sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ring[i % (QK_AHEAD + 1)], qb16[kk],
+                                                           kk == 0 ? f32x16{0.0f} : sacc[kb], 0, 0, 0);
+        if (i + QK_AHEAD < NQK) ring[(i + QK_AHEAD) % (QK_AHEAD + 1)] = ldk(i + QK_AHEAD);
+      }
+#pragma unroll
+      for (int i = 0; i < NQK; ++i) {
+        __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+        if (i + QK_AHEAD < NQK) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
+      }
+    } else {
+      auto ldk = [&](int i) {
+        const int kk = i >> 2;
+        const uint8_t* rowp = kl + (i & 3) * 32 * C::RB + krow_off;
+        const i32x4 lo = *(const i32x4*)(rowp + (((4 * kk + 2 * g) ^ kswz) << 4));
+        const i32x4 hi = *(const i32x4*)(rowp + (((4 * kk + 2 * g + 1) ^ kswz) << 4));
+        return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      };
+      i32x8 ring[QK_AHEAD + 1];
+#pragma unroll
+      for (int i = 0; i < QK_AHEAD; ++i) ring[i] = ldk(i);
+      __builtin_amdgcn_sched_barrier(0);  // the prologue reads go first
+#pragma unroll
+      for (int i = 0; i < NQK; ++i) {
+        const int kk = i >> 2, kb = i & 3;
+        sacc[kb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+            ring[i % (QK_AHEAD + 1)], qf8[kk], kk == 0 ? f32x16{0.0f} : sacc[kb], 0, 0, 0, 0, 0, 0);
+        if (i + QK_AHEAD < NQK) ring[(i + QK_AHEAD) % (QK_AHEAD + 1)] = ldk(i + QK_AHEAD);
+      }
+#pragma unroll
+      for (int i = 0; i < NQK; ++i) {
+        __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+        if (i + QK_AHEAD < NQK) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 2, 0);
+      }
+    }
+  };
+
+  // ---- O^T += V^T P^T for the tile whose V sits at vl and whose P is in pb/pf
+  auto pv = [&](const uint8_t* vl) {
+    const uint32_t vla = (uint32_t)(size_t)LDS_PTR(const uint8_t, vl);
+    if constexpr (DT == DT_BF16) {
+      // V^T operand: lane (d = i32 + 32 db, half g) needs keys
+      // 16 ks + 8 (r/4) + 4 g + r%4 (r = 0..7): two 4-key transposing reads;
+      // lane L16 of a 16-lane group addresses row 4 g + L16/4 (+8), columns
+      // 16 (G4%2) + 4 (L16%4) .. +3 of the 32-column block.  The swizzle of
+      // those rows equals that of vrow, so only the block db moves the lane's
+      // address; the key offset is an immediate.
+      const int vrow = 4 * (G4 >> 1) + (L16 >> 2);
+      const int vcolb = (16 * (G4 & 1) + 4 * (L16 & 3)) * 2;
+      uint32_t base[NDB];
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const int cb = 64 * db + vcolb;
+        base[db] = vla + vrow * C::RB + (((cb >> 4) ^ v_swz<DT, D>(vrow)) << 4) + (cb & 15);
+      }
+      // MFMA i covers (db = i / 8, ks = i % 8); V operands run PV_AHEAD ahead
+      auto ldv = [&](auto ic) {
+        constexpr int i = decltype(ic)::value;
+        const i32x2v lo = ds_read_tr16<(16 * (i & 7)) * C::RB>(base[i >> 3]);
+        const i32x2v hi = ds_read_tr16<(16 * (i & 7) + 8) * C::RB>(base[i >> 3]);
+        return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3));
+      };
+      constexpr int NPV = NDB * 8;
+      bf16x8 ring[PV_AHEAD + 1];
+      static_for<0, PV_AHEAD>([&](auto ic) { ring[decltype(ic)::value] = ldv(ic); });
+      static_for<0, NPV>([&](auto ic) {
+        constexpr int i = decltype(ic)::value;
+        // the reads of the PV_AHEAD - 1 later operands may still be in flight
+        lds_wait<2 * (i + PV_AHEAD <= NPV ? PV_AHEAD - 1 : NPV - 1 - i)>(ring[i % (PV_AHEAD + 1)]);
+        oacc[i >> 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ring[i % (PV_AHEAD + 1)], pb[i & 7], oacc[i >> 3], 0, 0, 0);
+        if constexpr (i + PV_AHEAD < NPV)
+          ring[(i + PV_AHEAD) % (PV_AHEAD + 1)] = ldv(std::integral_constant<int, i + PV_AHEAD>{});
+      });
+    } else {
+      // V^T operand: lane (d = i32 + 32 db, half g) needs, for byte r = 8 rd + e,
+      // key 32 (2 t2 + rd/2) + 16 (rd%2) + 8 (e/4) + 4 g + e%4: four 8-key
+      // transposing reads; lane L16 of a 16-lane group addresses row
+      // vrow = base + 8 (L16/8) + (L16/2)%4, columns d0 + 8 (L16%2) .. +7.
+      // The swizzle of those rows equals that of vrow.
+      const int vrow = 4 * (G4 >> 1) + 8 * (L16 >> 3) + ((L16 >> 1) & 3);
+      const int vcol = 16 * (G4 & 1) + 8 * (L16 & 1);
+      uint32_t base[NDB];
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const int cb = 32 * db + vcol;
+        base[db] = vla + vrow * C::RB + (((cb >> 4) ^ v_swz<DT, D>(vrow)) << 4) + (cb & 15);
+      }
+      // MFMA i covers (db = i / 2, t2 = i % 2); V operands run PV_AHEAD ahead
+      auto ldv = [&](auto ic) {
+        constexpr int i = decltype(ic)::value;
+        constexpr int t2 = i & 1;
+        const uint32_t a = base[i >> 1];
+        const i32x2v p0 = ds_read_tr8<(64 * t2) * C::RB>(a);
+        const i32x2v p1 = ds_read_tr8<(64 * t2 + 16) * C::RB>(a);
+        const i32x2v p2 = ds_read_tr8<(64 * t2 + 32) * C::RB>(a);
+        const i32x2v p3 = ds_read_tr8<(64 * t2 + 48) * C::RB>(a);
+        const i32x4 lo = __builtin_shufflevector(p0, p1, 0, 1, 2, 3);
+        const i32x4 hi = __builtin_shufflevector(p2, p3, 0, 1, 2, 3);
+        return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      };
+      constexpr int NPV = NDB * 2;
+      i32x8 ring[PV_AHEAD + 1];
+      static_for<0, PV_AHEAD>([&](auto ic) { ring[decltype(ic)::value] = ldv(ic); });
+      static_for<0, NPV>([&](auto ic) {
+        constexpr int i = decltype(ic)::value;
+        lds_wait<4 * (i + PV_AHEAD <= NPV ? PV_AHEAD - 1 : NPV - 1 - i)>(ring[i % (PV_AHEAD + 1)]);
+        oacc[i >> 1] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ring[i % (PV_AHEAD + 1)], pf[i & 1],
+                                                                       oacc[i >> 1], 0, 0, 0, 0, 0, 0);
+        if constexpr (i + PV_AHEAD < NPV)
+          ring[(i + PV_AHEAD) % (PV_AHEAD + 1)] = ldv(std::integral_constant<int, i + PV_AHEAD>{});
+      });
+    }
+  };
+
+  // ---- the scores of tile t become weights, the running state moves, and P
+  // is left in pb/pf for the PV product
+  auto softmax_tile = [&](int t) {
+    const int kt0 = t * BC;
+
+    // masking: causal diagonal and the ragged tail only
+    const bool need_mask = (CAUSAL && kt0 + BC - 1 > qw0) || (kt0 + BC > S);
+    if (need_mask) {
+      const int lim = (CAUSAL ? min(qrow, S - 1) : S - 1) - kt0 - 4 * g;
+      mask_beyond(sacc, lim, -INFINITY);
+    }
+
+    const bool probe_row = PROBE && b == p.pb && h == p.ph && qrow >= p.prow0 && qrow < p.prow0 + p.pnrows;
+    if constexpr (PROBE) {
+      if (probe_row) {
+        const size_t rbase = (size_t)(qrow - p.prow0) * S;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+            const int key = kt0 + kb * 32 + 8 * (j >> 2) + 4 * g + (j & 3);
+            if (key < S) p.s_out[rbase + key] = sacc[kb][j];
+          }
+      }
+    }
+
+    // running maximum (threshold 0: moves to the maximum so far)
+    const float mt = tile_max(sacc);
+    float ma, mb;
+    with_partner(mt, ma, mb);
+    const float m_new = max3(m_run, ma, mb);
+    const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * p.c1);
+    m_run = m_new;
+
+    // weights, in place over the scores
+    if constexpr (MODE != MODE_EXACT) {
+      const float nb2 = __builtin_fmaf(-m_new, p.c2, 2.0f * off);
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) sacc[kb][j] = h15_weight<MODE>(sacc[kb][j], p.c2, nb2);
+      if (need_mask) {
+        // masked keys carry weight 0 (the clamp alone would give 2^-126)
+        const int lim = (CAUSAL ? min(qrow, S - 1) : S - 1) - kt0 - 4 * g;
+        mask_beyond(sacc, lim, 0.0f);
+      }
+    } else {
+      const float nb1 = __builtin_fmaf(-m_new, p.c1, off);
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) sacc[kb][j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][j], p.c1, nb1));
+    }
+    l_part = l_part * alpha + tile_sum(sacc);
+    // skipping the rescale is exact when no row of the wave moved its max
+    if (__builtin_amdgcn_ballot_w64(alpha != 1.0f) != 0) {
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) oacc[db][j] *= alpha;
+    }
+
+    // P in the operand type
+    if constexpr (DT == DT_BF16) {
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks)
+#pragma unroll
+        for (int r = 0; r < 8; ++r) pb[ks][r] = (__bf16)sacc[ks >> 1][8 * (ks & 1) + r];
+    } else {
+#pragma unroll
+      for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+        for (int w4 = 0; w4 < 8; ++w4) {
+          const int kb = 2 * t2 + (w4 >> 2), j0 = 4 * (w4 & 3);
+          // the old value is fully overwritten by the two halves
+          uint32_t word = __float_as_uint(sacc[kb][j0]);
+          word = __builtin_amdgcn_cvt_pk_fp8_f32(sacc[kb][j0], sacc[kb][j0 + 1], word, false);
+          word = __builtin_amdgcn_cvt_pk_fp8_f32(sacc[kb][j0 + 2], sacc[kb][j0 + 3], word, true);
+          pf[t2][w4] = (int)word;
+        }
+    }
+    if constexpr (PROBE) {
+      if (probe_row) {
+        const size_t rbase = (size_t)(qrow - p.prow0) * S;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+            const int key = kt0 + kb * 32 + 8 * (j >> 2) + 4 * g + (j & 3);
+            if (key < S) {
+              uint32_t bits;
+              if constexpr (DT == DT_BF16) {
+                // read the bf16 bits through a 32-bit view of the operand
+                const u32x4 pw = __builtin_bit_cast(u32x4, pb[2 * kb + (j >> 3)]);
+                bits = (pw[(j & 7) >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+              } else {
+                bits = ((uint32_t)pf[kb >> 1][4 * (kb & 1) + (j >> 2)] >> (8 * (j & 3))) & 0xFFu;
+              }
+              p.w_out[rbase + key] = sacc[kb][j];
+              p.p_out[rbase + key] = bits;
+            }
+          }
+      }
+    }
+  };
+
+  // last tile holding a valid key for some row of this wave (-1: none)
+  const int last_act = !wave_live ? -1 : (CAUSAL ? min(ntiles - 1, (qw0 + WROWS - 1) / BC) : ntiles - 1);
+  // ---- one tile per step: copy in the next tile, then QK^T, weights, PV
+  stage_k(0, ALL_WAVES, 0);
+  stage_v(0, ALL_WAVES, 0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-
   for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < ntiles) stage_tile(t + 1, buf ^ 1);
-    const int kt0 = t * BC;
-    const bool active = wave_live && (!CAUSAL || kt0 <= qw0 + WROWS - 1);
-    if (active) {
-      const uint8_t* kl = smem + buf * C::BUF;
-      const uint8_t* vl = kl + C::TILE;
-
-      // ---- S^T = K Q^T for the 128 keys of the tile (4 blocks of 32 keys)
-      f32x16 sacc[4];
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb) sacc[kb] = f32x16{0.0f};
-      const int krow_off = i32 * C::RB;
-      const int kswz = k_swz<DT, D>(i32);  // == k_swz(kb * 32 + i32)
-      // MFMA i covers (kk = i / 4, kb = i % 4).  Its K operand is read from LDS
-      // QK_AHEAD MFMAs in advance into a ring of registers, and the schedule
-      // below keeps that order, so each MFMA finds its operand loaded.
-      constexpr int NQK = 4 * NKQ;
+    if (t + 1 < ntiles) {
+      stage_k(t + 1, ALL_WAVES, 0);
+      stage_v(t + 1, ALL_WAVES, 0);
+    }
+    if (t <= last_act) {
       __builtin_amdgcn_s_setprio(1);
-      if constexpr (DT == DT_BF16) {
-        auto ldk = [&](int i) {
-          const uint8_t* rowp = kl + (i & 3) * 32 * C::RB + krow_off;
-          return *(const bf16x8*)(rowp + (((2 * (i >> 2) + g) ^ kswz) << 4));
-        };
-        bf16x8 ring[QK_AHEAD + 1];
-#pragma unroll
-        for (int i = 0; i < QK_AHEAD; ++i) ring[i] = ldk(i);
-        __builtin_amdgcn_sched_barrier(0);  // the prologue reads go first
-#pragma unroll
-        for (int i = 0; i < NQK; ++i) {
-          const int kk = i >> 2, kb = i & 3;
-          sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ring[i % (QK_AHEAD + 1)], qb16[kk], sacc[kb], 0, 0, 0);
-          if (i + QK_AHEAD < NQK) ring[(i + QK_AHEAD) % (QK_AHEAD + 1)] = ldk(i + QK_AHEAD);
-        }
-#pragma unroll
-        for (int i = 0; i < NQK; ++i) {
-          __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
-          if (i + QK_AHEAD < NQK) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 1, 0);
-        }
-      } else {
-        auto ldk = [&](int i) {
-          const int kk = i >> 2;
-          const uint8_t* rowp = kl + (i & 3) * 32 * C::RB + krow_off;
-          const i32x4 lo = *(const i32x4*)(rowp + (((4 * kk + 2 * g) ^ kswz) << 4));
-          const i32x4 hi = *(const i32x4*)(rowp + (((4 * kk + 2 * g + 1) ^ kswz) << 4));
-          return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        };
-        i32x8 ring[QK_AHEAD + 1];
-#pragma unroll
-        for (int i = 0; i < QK_AHEAD; ++i) ring[i] = ldk(i);
-        __builtin_amdgcn_sched_barrier(0);  // the prologue reads go first
-#pragma unroll
-        for (int i = 0; i < NQK; ++i) {
-          const int kk = i >> 2, kb = i & 3;
-          sacc[kb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ring[i % (QK_AHEAD + 1)], qf8[kk], sacc[kb],
-                                                                     0, 0, 0, 0, 0, 0);
-          if (i + QK_AHEAD < NQK) ring[(i + QK_AHEAD) % (QK_AHEAD + 1)] = ldk(i + QK_AHEAD);
-        }
-#pragma unroll
-        for (int i = 0; i < NQK; ++i) {
-          __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
-          if (i + QK_AHEAD < NQK) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 2, 0);
-        }
-      }
+      qk(kbuf(t));
       __builtin_amdgcn_s_setprio(0);
-      // accumulator value j of block kb holds key kt0 + 32 kb + 8 (j/4) + 4 g + j%4
-
-      // ---- masking: causal diagonal and the ragged tail only
-      const bool need_mask = (CAUSAL && kt0 + BC - 1 > qw0) || (kt0 + BC > S);
-      if (need_mask) {
-        const int lim = (CAUSAL ? min(qrow, S - 1) : S - 1) - kt0 - 4 * g;
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-          for (int j = 0; j < 16; ++j)
-            if (kb * 32 + 8 * (j >> 2) + (j & 3) > lim) sacc[kb][j] = -INFINITY;
-      }
-
-      const bool probe_row = PROBE && b == p.pb && h == p.ph && qrow >= p.prow0 &&
-                             qrow < p.prow0 + p.pnrows;
-      if constexpr (PROBE) {
-        if (probe_row) {
-          const size_t rbase = (size_t)(qrow - p.prow0) * S;
-#pragma unroll
-          for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-            for (int j = 0; j < 16; ++j) {
-              const int key = kt0 + kb * 32 + 8 * (j >> 2) + 4 * g + (j & 3);
-              if (key < S) p.s_out[rbase + key] = sacc[kb][j];
-            }
-        }
-      }
-
-      // ---- running maximum (threshold 0: moves to the maximum so far)
-      const float mt = tile_max(sacc);
-      const float m_new = max3(m_run, mt, __shfl_xor(mt, 32));
-      const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * p.c1);
-      m_run = m_new;
-
-      // ---- weights, in place over the scores
-      float tsum = 0.0f;
-      if constexpr (MODE != MODE_EXACT) {
-        const float nb2 = __builtin_fmaf(-m_new, p.c2, 2.0f * off);
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            const float w = h15_weight<MODE>(sacc[kb][j], p.c2, nb2);
-            sacc[kb][j] = w;
-          }
-        if (need_mask) {
-          // masked keys carry weight 0 (the clamp alone would give 2^-126).
-          // The limit is laundered through an empty asm so the compiler does
-          // not share these comparisons with the score masking above, which
-          // would keep 64 masks live across every tile.
-          int lim = (CAUSAL ? min(qrow, S - 1) : S - 1) - kt0 - 4 * g;
-          asm volatile("" : "+v"(lim));
-#pragma unroll
-          for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-            for (int j = 0; j < 16; ++j)
-              if (kb * 32 + 8 * (j >> 2) + (j & 3) > lim) sacc[kb][j] = 0.0f;
-        }
-        tsum = tile_sum(sacc);
-      } else {
-        const float nb1 = __builtin_fmaf(-m_new, p.c1, off);
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            sacc[kb][j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][j], p.c1, nb1));
-          }
-        tsum = tile_sum(sacc);
-      }
-      l_part = l_part * alpha + tsum;
-      // skipping the rescale is exact when no row of the wave moved its max
-      if (__builtin_amdgcn_ballot_w64(alpha != 1.0f) != 0) {
-#pragma unroll
-        for (int db = 0; db < NDB; ++db)
-#pragma unroll
-          for (int j = 0; j < 16; ++j) oacc[db][j] *= alpha;
-      }
-
-      // ---- P in the operand type, then O^T += V^T P^T
-      if constexpr (DT == DT_BF16) {
-        bf16x8 pb[8];
-#pragma unroll
-        for (int ks = 0; ks < 8; ++ks)
-#pragma unroll
-          for (int r = 0; r < 8; ++r) pb[ks][r] = (__bf16)sacc[ks >> 1][8 * (ks & 1) + r];
-        if constexpr (PROBE) {
-          if (probe_row) {
-            const size_t rbase = (size_t)(qrow - p.prow0) * S;
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-              for (int j = 0; j < 16; ++j) {
-                const int key = kt0 + kb * 32 + 8 * (j >> 2) + 4 * g + (j & 3);
-                if (key < S) {
-                  const __bf16 pv = pb[2 * kb + (j >> 3)][j & 7];
-                  p.w_out[rbase + key] = sacc[kb][j];
-                  p.p_out[rbase + key] = (uint32_t)__builtin_bit_cast(uint16_t, pv);
-                }
-              }
-          }
-        }
-        // V^T operand: lane (d = i32 + 32 db, half g) needs keys
-        // 16 ks + 8 (r/4) + 4 g + r%4 (r = 0..7): two 4-key transposing reads;
-        // lane L16 of a 16-lane group addresses row 4 g + L16/4 (+8), columns
-        // 16 (G4%2) + 4 (L16%4) .. +3 of the 32-column block.
-        const int vrow = 4 * (G4 >> 1) + (L16 >> 2);
-        const int vcolb = (16 * (G4 & 1) + 4 * (L16 & 3)) * 2;
-        // MFMA i covers (db = i / 8, ks = i % 8); V operands run PV_AHEAD ahead
-        auto ldv = [&](int i) {
-          const int r0 = 16 * (i & 7) + vrow, r1 = r0 + 8;
-          const int cb = 64 * (i >> 3) + vcolb;
-          const uint8_t* a0 = vl + r0 * C::RB + (((cb >> 4) ^ v_swz<DT, D>(r0)) << 4) + (cb & 15);
-          const uint8_t* a1 = vl + r1 * C::RB + (((cb >> 4) ^ v_swz<DT, D>(r1)) << 4) + (cb & 15);
-          const bf16x4v lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(LDS_PTR(bf16x4v, a0));
-          const bf16x4v hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(LDS_PTR(bf16x4v, a1));
-          return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        };
-        constexpr int NPV = NDB * 8;
-        bf16x8 ring[PV_AHEAD + 1];
-        __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-        for (int i = 0; i < PV_AHEAD; ++i) ring[i] = ldv(i);
-        __builtin_amdgcn_sched_barrier(0);  // the prologue reads go first
-#pragma unroll
-        for (int i = 0; i < NPV; ++i) {
-          oacc[i >> 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ring[i % (PV_AHEAD + 1)], pb[i & 7], oacc[i >> 3], 0, 0, 0);
-          if (i + PV_AHEAD < NPV) ring[(i + PV_AHEAD) % (PV_AHEAD + 1)] = ldv(i + PV_AHEAD);
-        }
-#pragma unroll
-        for (int i = 0; i < NPV; ++i) {
-          __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 1);
-          if (i + PV_AHEAD < NPV) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 2, 1);
-        }
-        __builtin_amdgcn_s_setprio(0);
-      } else {
-        i32x8 pf[2];
-#pragma unroll
-        for (int t2 = 0; t2 < 2; ++t2)
-#pragma unroll
-          for (int w4 = 0; w4 < 8; ++w4) {
-            const int kb = 2 * t2 + (w4 >> 2), j0 = 4 * (w4 & 3);
-            // the old value is fully overwritten by the two halves
-            uint32_t word = __float_as_uint(sacc[kb][j0]);
-            word = __builtin_amdgcn_cvt_pk_fp8_f32(sacc[kb][j0], sacc[kb][j0 + 1], word, false);
-            word = __builtin_amdgcn_cvt_pk_fp8_f32(sacc[kb][j0 + 2], sacc[kb][j0 + 3], word, true);
-            pf[t2][w4] = (int)word;
-          }
-        if constexpr (PROBE) {
-          if (probe_row) {
-            const size_t rbase = (size_t)(qrow - p.prow0) * S;
-#pragma unroll
-            for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-              for (int j = 0; j < 16; ++j) {
-                const int key = kt0 + kb * 32 + 8 * (j >> 2) + 4 * g + (j & 3);
-                if (key < S) {
-                  const uint32_t word = (uint32_t)pf[kb >> 1][4 * (kb & 1) + (j >> 2)];
-                  p.w_out[rbase + key] = sacc[kb][j];
-                  p.p_out[rbase + key] = (word >> (8 * (j & 3))) & 0xFFu;
-                }
-              }
-          }
-        }
-        // V^T operand: lane (d = i32 + 32 db, half g) needs, for byte r = 8 rd + e,
-        // key 32 (2 t2 + rd/2) + 16 (rd%2) + 8 (e/4) + 4 g + e%4: four 8-key
-        // transposing reads; lane L16 of a 16-lane group addresses row
-        // base + 8 (L16/8) + (L16/2)%4, columns d0 + 8 (L16%2) .. +7.
-        const int vrow = 4 * (G4 >> 1) + 8 * (L16 >> 3) + ((L16 >> 1) & 3);
-        const int vcol = 16 * (G4 & 1) + 8 * (L16 & 1);
-        // MFMA i covers (db = i / 2, t2 = i % 2); V operands run PV_AHEAD ahead
-        auto ldv = [&](int i) {
-          const int db = i >> 1, t2 = i & 1;
-          i32x2v part[4];
-#pragma unroll
-          for (int rd = 0; rd < 4; ++rd) {
-            const int row = 32 * (2 * t2 + (rd >> 1)) + 16 * (rd & 1) + vrow;
-            const int cb = 32 * db + vcol;
-            const uint8_t* a = vl + row * C::RB + (((cb >> 4) ^ v_swz<DT, D>(row)) << 4) + (cb & 15);
-            part[rd] = __builtin_amdgcn_ds_read_tr8_b64_v2i32(LDS_PTR(i32x2v, a));
-          }
-          const i32x4 lo = __builtin_shufflevector(part[0], part[1], 0, 1, 2, 3);
-          const i32x4 hi = __builtin_shufflevector(part[2], part[3], 0, 1, 2, 3);
-          return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        };
-        constexpr int NPV = NDB * 2;
-        i32x8 ring[PV_AHEAD + 1];
-        __builtin_amdgcn_s_setprio(1);
-#pragma unroll
-        for (int i = 0; i < PV_AHEAD; ++i) ring[i] = ldv(i);
-        __builtin_amdgcn_sched_barrier(0);  // the prologue reads go first
-#pragma unroll
-        for (int i = 0; i < NPV; ++i) {
-          oacc[i >> 1] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ring[i % (PV_AHEAD + 1)], pf[i & 1],
-                                                                         oacc[i >> 1], 0, 0, 0, 0, 0, 0);
-          if (i + PV_AHEAD < NPV) ring[(i + PV_AHEAD) % (PV_AHEAD + 1)] = ldv(i + PV_AHEAD);
-        }
-#pragma unroll
-        for (int i = 0; i < NPV; ++i) {
-          __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 1);
-          if (i + PV_AHEAD < NPV) __builtin_amdgcn_sched_group_barrier(SG_DS_READ, 4, 1);
-        }
-        __builtin_amdgcn_s_setprio(0);
-      }
+      softmax_tile(t);
+      __builtin_amdgcn_s_setprio(1);
+      pv(vbuf(t));
+      __builtin_amdgcn_s_setprio(0);
     }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
@@ -535,7 +622,9 @@ __global__ __launch_bounds__(NTHREADS) void attn_fwd_kernel(Params p) {
 
   // ---- epilogue: O = acc / l * v_descale (bf16), LSE
   if (!wave_live) return;
-  const float l = l_part + __shfl_xor(l_part, 32);
+  float la, lb;
+  with_partner(l_part, la, lb);
+  const float l = la + lb;
   if (qrow >= S) return;
   const float inv = p.vd / l;
   uint16_t* orow = p.o + (q_head + qrow) * (size_t)D;
@@ -571,8 +660,8 @@ __global__ void probe_fill(float* s, float* w, uint32_t* pbits, size_t n) {
 template <int DT, int D, bool CAUSAL, int MODE, bool PROBE>
 hipError_t launch_one(const Params& p, hipStream_t st) {
   const unsigned grid = (unsigned)(p.nqb * p.B * p.Hq);
-  hipLaunchKernelGGL((attn_fwd_kernel<DT, D, CAUSAL, MODE, PROBE>), dim3(grid), dim3(NTHREADS), 0,
-                     st, p);
+  hipLaunchKernelGGL((attn_fwd_kernel<DT, D, CAUSAL, MODE, PROBE>), dim3(grid), dim3(Cfg<DT, D>::NW * 64), 0, st,
+                     p);
   return hipGetLastError();
 }
 
@@ -616,6 +705,11 @@ int kernel_mode(int dtype, int exp_mode, int d, float c2) {
   return MODE_H15;
 }
 
+// query rows per workgroup for an operand type
+int row_block(int dtype) {
+  return (dtype == ATTN_FP8_E4M3 ? Cfg<DT_FP8, 128>::BR : Cfg<DT_BF16, 128>::BR);
+}
+
 int fill_params(Params& p, const void* q, const void* k, const void* v, void* o, float* lse, int B,
                 int Hq, int Hkv, int S, int d, float scale, int dtype, int exp_mode,
                 const attn_opts* opts) {
@@ -657,7 +751,7 @@ int fill_params(Params& p, const void* q, const void* k, const void* v, void* o,
   p.c1 = (float)((double)scale * (double)qd * (double)kd * 1.4426950408889634);
   p.c2 = 2.0f * p.c1;
   p.vd = vd;
-  p.nqb = (S + BR - 1) / BR;
+  p.nqb = (S + row_block(dtype) - 1) / row_block(dtype);
   p.remap = ((B * Hkv) % 8 == 0) ? 1 : 0;
   return ATTN_OK;
 }
