@@ -8,8 +8,10 @@ C, fp64 accumulation), this module only marshals numpy arrays through ctypes.
 Paper: "Approximating Softmax in Pretrained LLMs: Model Sensitivity and Kernel
 Acceleration".  Modes follow App. A.1 Eq. (exact-attention) (EXACT),
 Sec. 5.2 Eq. (m-h15) with App. B.1 "Implementation" and the per-tile running
-max of App. B.2 (H15_TILE), the whole-row control of Table B2 (H15_WHOLEROW)
-and App. A.6 Eq. (rowmax-pot) (ROWMAX_POT).
+max of App. B.2 (H15_TILE), the whole-row control of Table B2 (H15_WHOLEROW),
+App. A.6 Eq. (rowmax-pot) (ROWMAX_POT) and the finer input-rounding family
+S(Q_{2^-k}(x)) of App. B.2 "Exponential-map ablation" with the per-tile running
+max (SQ4_TILE for k = 2, SQ8_TILE for k = 3).
 """
 from __future__ import annotations
 
@@ -22,7 +24,9 @@ import numpy as np
 from .build import build as _build, LIB_PATH
 
 BF16, FP8_E4M3 = 0, 1
-EXACT, H15_TILE, H15_WHOLEROW, ROWMAX_POT, EXACT_TILE = 0, 1, 2, 3, 4
+EXACT, H15_TILE, H15_WHOLEROW, ROWMAX_POT, EXACT_TILE, SQ4_TILE, SQ8_TILE = 0, 1, 2, 3, 4, 5, 6
+# input-rounding exponent k of each tiled mode (Rowmax-H15 is k = 1)
+MODE_K = {H15_TILE: 1, H15_WHOLEROW: 1, SQ4_TILE: 2, SQ8_TILE: 3}
 
 _lib = None
 
@@ -49,6 +53,16 @@ def lib() -> ctypes.CDLL:
     L.oracle_h15_ideal.restype = c_d
     L.oracle_h15_exhaustive.argtypes = [c_f, c_f, ctypes.POINTER(c_i64)]
     L.oracle_h15_exhaustive.restype = c_i64
+    L.oracle_sq_weight.argtypes = [c_f, c_i]
+    L.oracle_sq_weight.restype = c_f
+    L.oracle_sq_ideal.argtypes = [c_d, c_i]
+    L.oracle_sq_ideal.restype = c_d
+    L.oracle_sq_exhaustive.argtypes = [c_f, c_f, c_i, ctypes.POINTER(c_i64)]
+    L.oracle_sq_exhaustive.restype = c_i64
+    L.oracle_sq_count_mismatch.argtypes = [c_p, c_i64, c_i]
+    L.oracle_sq_count_mismatch.restype = c_i64
+    L.oracle_sq_row_from_logits.argtypes = [c_p, c_i, c_i, c_i, c_f, c_i, c_i, c_d, c_i, c_i, c_p, c_p, c_p]
+    L.oracle_sq_row_from_logits.restype = c_i
     L.oracle_c1.argtypes = [c_d, c_d, c_d]
     L.oracle_c1.restype = c_f
     L.oracle_h15_row_from_logits.argtypes = [c_p, c_i, c_i, c_i, c_f, c_i, c_i, c_d, c_i, c_p, c_p, c_p]
@@ -99,6 +113,29 @@ def h15_exhaustive(lo: float, hi: float) -> tuple[int, int]:
     return int(bad), int(n.value)
 
 
+def sq_weight(y: float, k: int) -> float:
+    """S(Q_{2^-k}) realisation (App. B.2 ablation): add 0x4B400000, shift by 23 - k; y = 2^k x."""
+    return lib().oracle_sq_weight(float(y), int(k))
+
+
+def sq_ideal(y: float, k: int) -> float:
+    """S(Q_{2^-k}(x)) from the definitions of S and Q, on y = 2^k x (no clamp)."""
+    return lib().oracle_sq_ideal(float(y), int(k))
+
+
+def sq_exhaustive(lo: float, hi: float, k: int) -> tuple[int, int]:
+    """Compare the two forms over every fp32 value in [lo, hi]; (mismatches, count)."""
+    n = ctypes.c_int64(0)
+    bad = lib().oracle_sq_exhaustive(float(lo), float(hi), int(k), ctypes.byref(n))
+    return int(bad), int(n.value)
+
+
+def sq_count_mismatch(x: np.ndarray, k: int) -> int:
+    """Realisation vs S(Q_{2^-k}) on base-two exponents x (clamped at -126); mismatches."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    return int(lib().oracle_sq_count_mismatch(_ptr(x), int(x.shape[0]), int(k)))
+
+
 def c1(scale: float, qd: float = 1.0, kd: float = 1.0) -> float:
     """Base-two exponent scale of a raw logit, fp32(scale*qd*kd*log2 e)."""
     return lib().oracle_c1(float(scale), float(qd), float(kd))
@@ -119,6 +156,21 @@ def h15_row_from_logits(s: np.ndarray, i: int, causal: bool, c1_: float, dtype: 
                                           ctypes.byref(lse))
     if rc != 0:
         raise ValueError("oracle_h15_row_from_logits: invalid arguments")
+    return w, p, lse.value
+
+
+def sq_row_from_logits(s: np.ndarray, i: int, causal: bool, c1_: float, dtype: int, Bc: int, k: int,
+                       tau: float = 0.0):
+    """As h15_row_from_logits for the weight S(Q_{2^-k}) (k = 1 is Rowmax-H15)."""
+    s = np.ascontiguousarray(s, dtype=np.float32)
+    S = s.shape[0]
+    w = np.zeros(S, np.float32)
+    p = np.zeros(S, np.uint32)
+    lse = ctypes.c_double(0.0)
+    rc = lib().oracle_sq_row_from_logits(_ptr(s), S, int(i), int(bool(causal)), float(c1_), int(dtype),
+                                         int(Bc), float(tau), 0, int(k), _ptr(w), _ptr(p), ctypes.byref(lse))
+    if rc != 0:
+        raise ValueError("oracle_sq_row_from_logits: invalid arguments")
     return w, p, lse.value
 
 

@@ -19,6 +19,9 @@
  *                                          rescale threshold 0 (FP8 path)
  *   App. B.2, Table B2                     offline whole-row control
  *   App. A.6 Eq. (rowmax-pot)              Rowmax-PoT, K_max = 20
+ *   App. B.2 "Exponential-map ablation"    the finer input-rounding family
+ *                                          S(Q_{2^-k}(x)), k = 2, 3, realised
+ *                                          with 2^k and a shift by 23 - k
  *
  * Precision policy: everything the paper leaves to "exact" arithmetic is done
  * in fp64 from the exactly decoded stored operands (bf16 values, or e4m3 codes
@@ -46,8 +49,10 @@ enum {
     OR_H15_TILE = 1,     /* Rowmax-H15 with the per-tile running max (App. B.2) */
     OR_H15_WHOLEROW = 2, /* Rowmax-H15 anchored at the final whole-row max */
     OR_ROWMAX_POT = 3,   /* App. A.6 Rowmax-PoT, whole row, K_max = 20 */
-    OR_EXACT_TILE = 4    /* diagnostic: exact exp2 inside the same tile loop,
+    OR_EXACT_TILE = 4,   /* diagnostic: exact exp2 inside the same tile loop,
                             with the kernel's P storage rounding */
+    OR_SQ4_TILE = 5,     /* S(Q_{1/4}(x)) with the per-tile running max */
+    OR_SQ8_TILE = 6      /* S(Q_{1/8}(x)) with the per-tile running max */
 };
 
 static uint32_t f2u(float f) { uint32_t u; memcpy(&u, &f, 4); return u; }
@@ -159,6 +164,77 @@ int64_t oracle_h15_exhaustive(float lo, float hi, int64_t* count)
     return bad;
 }
 
+/* ---- the S(Q_{2^-k}) family (App. B.2 "Exponential-map ablation") ------ */
+
+/* The realisation that the paper's bit-level test describes: the FP32 add of
+ * 0x4B400000 and shift of App. B.1 with 2^k in place of the doubling and a
+ * left shift by 23 - k.  y is 2^k x in FP32; the clamp x >= -126 becomes
+ * y >= -126 * 2^k.  k = 1 is Rowmax-H15.  Valid for 0 <= k <= 22 and
+ * |y| < 2^22. */
+float oracle_sq_weight(float y, int k)
+{
+    const float lo = -126.0f * (float)(1 << k);
+    volatile float yc = (y < lo) ? lo : y;
+    volatile float t = yc + 12582912.0f;
+    uint32_t u = (f2u(t) << (23 - k)) + 0x3F800000u;
+    return u2f(u);
+}
+
+/* The ideal operator written from its two definitions: the unshifted
+ * Schraudolph map S(q) = 2^floor(q) (1 + q - floor(q)) (App. B.1, "Relation
+ * to classical bit-level exponentiation") applied to the quantised input
+ * Q_{2^-k}(x) = 2^-k RNE(2^k x).  The argument is y = 2^k x. */
+double oracle_sq_ideal(double y, int k)
+{
+    double q = ldexp(nearbyint(y), -k); /* RNE in the default rounding mode */
+    double fl = floor(q);
+    return ldexp(1.0 + (q - fl), (int)fl);
+}
+
+/* Exhaustive comparison of the two forms above over every fp32 y in
+ * [lo, hi], both taken after the clamp at -126 * 2^k.  Returns the number of
+ * mismatching bit patterns; *count receives the number of values tested. */
+int64_t oracle_sq_exhaustive(float lo, float hi, int k, int64_t* count)
+{
+    int64_t bad = 0, n = 0;
+    const double clamp = -126.0 * (double)(1 << k);
+    uint32_t hi_bits = hi >= 0 ? f2u(hi) : 0;
+    uint32_t lo_mag = lo <= 0 ? (f2u(lo) & 0x7FFFFFFFu) : 0;
+    int64_t npos = hi >= 0 ? (int64_t)hi_bits + 1 : 0;
+    int64_t nneg = lo <= 0 ? (int64_t)lo_mag + 1 : 0;
+    int64_t total = npos + nneg;
+#pragma omp parallel for reduction(+ : bad, n) schedule(static)
+    for (int64_t idx = 0; idx < total; idx++) {
+        uint32_t bits = idx < npos ? (uint32_t)idx : (0x80000000u | (uint32_t)(idx - npos));
+        float y = u2f(bits);
+        if (y < lo || y > hi) continue;
+        double yc = (double)y < clamp ? clamp : (double)y;
+        float want = (float)oracle_sq_ideal(yc, k);
+        float got = oracle_sq_weight(y, k);
+        n++;
+        if (f2u(want) != f2u(got)) bad++;
+    }
+    if (count) *count = n;
+    return bad;
+}
+
+/* The same comparison on a given list of base-two exponents x (fp32): both
+ * forms are evaluated at y = 2^k x after the clamp x >= -126 (the scaling by
+ * 2^k is exact).  Returns the number of mismatching bit patterns. */
+int64_t oracle_sq_count_mismatch(const float* x, int64_t n, int k)
+{
+    int64_t bad = 0;
+#pragma omp parallel for reduction(+ : bad) schedule(static)
+    for (int64_t i = 0; i < n; i++) {
+        float xc = x[i] < -126.0f ? -126.0f : x[i];
+        float y = ldexpf(xc, k);
+        float want = (float)oracle_sq_ideal((double)y, k);
+        float got = oracle_sq_weight(y, k);
+        if (f2u(want) != f2u(got)) bad++;
+    }
+    return bad;
+}
+
 /* The exponent-path constant: the base-two scale applied to a raw logit,
  * c1 = fp32(scale * q_descale * k_descale * log2(e)), products taken in
  * double in this order.  The H15 path uses c2 = 2*c1 (App. B.1: separate,
@@ -184,10 +260,12 @@ float oracle_c1(double scale, double qd, double kd)
  *   jend   number of valid keys (keys 0 .. jend-1), >= 1
  * Outputs (each optional): o[d] (unscaled by vd), *lse, w[S], p[S]. */
 static void tiled_row(const float* s, const double* vrows, int S, int d, int jend, float c1,
-                      int off, int Bc, double tau, int dtype, int exact_exp, double vd,
+                      int off, int Bc, double tau, int dtype, int exact_exp, int kq, double vd,
                       double* o, double* lse, float* w, uint32_t* p, double* acc)
 {
-    const float c2 = 2.0f * c1; /* exact doubling */
+    /* the input-rounding exponent k: 1 for Rowmax-H15 (c2 = 2 c1, shift 22),
+     * 2 or 3 for S(Q_{2^-k}) (2^k c1, shift 23 - k); the scaling by 2^k is exact */
+    const float ck = ldexpf(c1, kq);
     float m = -INFINITY;
     double l = 0.0;
     if (acc) for (int c = 0; c < d; c++) acc[c] = 0.0;
@@ -206,12 +284,13 @@ static void tiled_row(const float* s, const double* vrows, int S, int d, int jen
         double alpha = (m == -INFINITY) ? 0.0 : exp2(((double)m - (double)m_new) * (double)c1);
         l *= alpha;
         if (acc) for (int c = 0; c < d; c++) acc[c] *= alpha;
-        float nb2 = fmaf(-m_new, c2, (float)(2 * off));
+        float nbk = fmaf(-m_new, ck, (float)((1 << kq) * off));
         float nb1 = fmaf(-m_new, c1, (float)off);
         for (int j = t0; j < v1; j++) {
             float wj;
             if (exact_exp) wj = (float)exp2((double)fmaf(s[j], c1, nb1));
-            else wj = oracle_h15_weight(fmaf(s[j], c2, nb2));
+            else if (kq == 1) wj = oracle_h15_weight(fmaf(s[j], ck, nbk));
+            else wj = oracle_sq_weight(fmaf(s[j], ck, nbk), kq);
             uint32_t pb;
             double pv;
             if (dtype == OR_BF16) {
@@ -236,16 +315,24 @@ static void tiled_row(const float* s, const double* vrows, int S, int d, int jen
 
 /* W and P of one row from given fp32 logits (for bit-exact comparison with
  * values that another implementation stored for the same logits). */
+int oracle_sq_row_from_logits(const float* s, int S, int i, int causal, float c1, int dtype,
+                              int Bc, double tau, int exact_exp, int k, float* w_out,
+                              uint32_t* p_out, double* lse_out)
+{
+    if (S <= 0 || Bc <= 0 || i < 0 || i >= S || k < 1 || k > 3) return -1;
+    int off = dtype == OR_FP8_E4M3 ? 8 : 0;
+    int jend = causal ? i + 1 : S;
+    tiled_row(s, NULL, S, 0, jend, c1, off, Bc, tau, dtype, exact_exp, k, 1.0, NULL, lse_out, w_out,
+              p_out, NULL);
+    return 0;
+}
+
 int oracle_h15_row_from_logits(const float* s, int S, int i, int causal, float c1, int dtype,
                                int Bc, double tau, int exact_exp, float* w_out, uint32_t* p_out,
                                double* lse_out)
 {
-    if (S <= 0 || Bc <= 0 || i < 0 || i >= S) return -1;
-    int off = dtype == OR_FP8_E4M3 ? 8 : 0;
-    int jend = causal ? i + 1 : S;
-    tiled_row(s, NULL, S, 0, jend, c1, off, Bc, tau, dtype, exact_exp, 1.0, NULL, lse_out, w_out,
-              p_out, NULL);
-    return 0;
+    return oracle_sq_row_from_logits(s, S, i, causal, c1, dtype, Bc, tau, exact_exp, 1, w_out,
+                                     p_out, lse_out);
 }
 
 /* ---- full attention --------------------------------------------------- */
@@ -268,9 +355,9 @@ int oracle_attn(const void* q, const void* k, const void* v, int dtype, double q
                 int Bc, double tau, const int64_t* rows, int64_t nrows, double* o, double* lse)
 {
     if (!q || !k || !v || !o || B <= 0 || Hq <= 0 || Hkv <= 0 || S <= 0 || d <= 0) return -1;
-    if (Hq % Hkv != 0 || (dtype != OR_BF16 && dtype != OR_FP8_E4M3) || mode < 0 || mode > 4)
+    if (Hq % Hkv != 0 || (dtype != OR_BF16 && dtype != OR_FP8_E4M3) || mode < 0 || mode > 6)
         return -1;
-    if ((mode == OR_H15_TILE || mode == OR_EXACT_TILE) && Bc <= 0) return -1;
+    if (mode != OR_EXACT && mode != OR_ROWMAX_POT && mode != OR_H15_WHOLEROW && Bc <= 0) return -1;
     const int64_t total = (int64_t)B * Hq * S;
     if (!rows) nrows = total;
     const int group = Hq / Hkv;
@@ -328,8 +415,9 @@ int oracle_attn(const void* q, const void* k, const void* v, int dtype, double q
             if (lse) lse[r] = sigma * smax + log(den);
         } else {
             int tile = (mode == OR_H15_WHOLEROW) ? S : Bc;
-            tiled_row(s32, vrows, S, d, jend, c1, off, tile, tau, dtype, mode == OR_EXACT_TILE, vd,
-                      orow, lse ? &lse[r] : NULL, NULL, NULL, acc);
+            int kq = mode == OR_SQ4_TILE ? 2 : mode == OR_SQ8_TILE ? 3 : 1;
+            tiled_row(s32, vrows, S, d, jend, c1, off, tile, tau, dtype, mode == OR_EXACT_TILE, kq,
+                      vd, orow, lse ? &lse[r] : NULL, NULL, NULL, acc);
         }
         free(qrow); free(sexact); free(vrows); free(acc); free(s32);
     }

@@ -1,0 +1,247 @@
+"""Pins of the oracle's finer input-rounding weights S(Q_{2^-k}(x)) (App. B.2,
+"Exponential-map ablation"): Q_{2^-k}(x) = 2^-k RNE(2^k x) fed to the
+unshifted Schraudolph map S(q) = 2^floor(q) (1 + q - floor(q)) of App. B.1,
+realised by the add of 0x4B400000 with 2^k in place of the doubling and a left
+shift by 23 - k.  Checked against the paper's own test set for every k it
+lists, exhaustively for the kernel's k = 2, 3, and against closed forms and
+invariants; never against itself."""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+
+
+def paper_test_inputs() -> np.ndarray:
+    """The paper's 2,295,040 inputs in [-126, 0]: 2,000,000 uniform draws, the
+    integers 0 .. -126 and every multiple of 7 * 2^-14 (which include RNE ties
+    for every k)."""
+    rng = np.random.default_rng(2609)
+    uni = rng.uniform(-126.0, 0.0, 2_000_000).astype(np.float32)
+    ints = -np.arange(0, 127, dtype=np.float32)
+    step = 7.0 * 2.0 ** -14
+    mult = (-np.arange(0, int(126 / step) + 1, dtype=np.float64) * step).astype(np.float32)
+    return np.concatenate([uni, ints, mult])
+
+
+def test_paper_test_set_size():
+    assert paper_test_inputs().shape[0] == 2_295_040
+
+
+@pytest.mark.parametrize("k", range(0, 14))
+def test_bit_form_matches_ideal_on_paper_inputs(k):
+    # the paper reports bit-for-bit agreement for each k = 0..13 on these inputs
+    assert oracle.sq_count_mismatch(paper_test_inputs(), k) == 0
+
+
+@pytest.mark.parametrize("k", [2, 3])
+def test_exhaustive_for_kernel_orders(k):
+    # every fp32 y = 2^k x from below the clamp to beyond the FP8 offset 8
+    lo, hi = -126.0 * 2 ** k - 4.0 * 2 ** k, (8.0 + 2.0) * 2 ** k
+    bad, n = oracle.sq_exhaustive(lo, hi, k)
+    assert n > 2_200_000_000
+    assert bad == 0
+
+
+def test_order_one_is_rowmax_h15():
+    rng = np.random.default_rng(1)
+    ys = np.concatenate([rng.uniform(-300.0, 40.0, 200_000), np.arange(-260.0, 30.0, 0.25)]).astype(np.float32)
+    for y in ys[::37]:
+        assert oracle.sq_weight(float(y), 1) == oracle.h15_weight(float(y))
+
+
+@pytest.mark.parametrize("k", [2, 3])
+def test_clamp_at_minus_126_octaves(k):
+    for x in (-126.0, -126.3, -127.0, -500.0, -1e9):
+        assert oracle.sq_weight(x * 2 ** k, k) == 2.0 ** -126
+
+
+@pytest.mark.parametrize("k", [2, 3])
+def test_integer_exponents_are_exact_powers_of_two(k):
+    for x in range(-126, 12):
+        assert oracle.sq_weight(float(x * 2 ** k), k) == 2.0 ** x
+
+
+@pytest.mark.parametrize("k", [2, 3])
+def test_lattice_points_closed_form(k):
+    # x = a + f / 2^k on the input lattice: S gives 2^a (1 + f / 2^k) exactly
+    for a in range(-126, 9):
+        for f in range(2 ** k):
+            y = float(a * 2 ** k + f)
+            assert oracle.sq_weight(y, k) == 2.0 ** a * (1 + f / 2 ** k)
+
+
+@pytest.mark.parametrize("k", [2, 3])
+def test_mantissa_has_at_most_k_bits(k):
+    rng = np.random.default_rng(3)
+    ys = rng.uniform(-126.0 * 2 ** k, 8.0 * 2 ** k, 50_000).astype(np.float32)
+    mask = (1 << (23 - k)) - 1
+    for y in ys:
+        bits = int(np.array([oracle.sq_weight(float(y), k)], np.float32).view(np.uint32)[0])
+        assert bits & mask == 0
+
+
+@pytest.mark.parametrize("k", [2, 3])
+def test_rne_ties_go_to_even(k):
+    # y = n + 1/2: RNE picks the even neighbour
+    for n in range(-40, 20):
+        y = n + 0.5
+        even = n if n % 2 == 0 else n + 1
+        assert oracle.sq_weight(y, k) == oracle.sq_weight(float(even), k)
+
+
+@pytest.mark.parametrize("k", [2, 3])
+def test_monotone_in_the_exponent(k):
+    ys = np.sort(np.random.default_rng(4).uniform(-126.0 * 2 ** k, 8.0 * 2 ** k, 20_000)).astype(np.float32)
+    w = np.array([oracle.sq_weight(float(y), k) for y in ys])
+    assert np.all(np.diff(w) >= 0)
+
+
+@pytest.mark.parametrize("k", [2, 3])
+def test_octave_error_envelope(k):
+    # App. B.1's split of the octave error: input rounding |q - x| <= 2^-(k+1)
+    # plus the interpolation term log2 S(q) - q, which is 0 at integers and at
+    # most max over the lattice fractions f of log2(1 + f) - f.
+    interp = max(math.log2(1 + f / 2 ** k) - f / 2 ** k for f in range(2 ** k))
+    lo, hi = -2.0 ** -(k + 1), 2.0 ** -(k + 1) + interp
+    xs = np.random.default_rng(5).uniform(-120.0, 0.0, 100_000)
+    for x in xs[::7]:
+        y = np.float32(x * 2 ** k)
+        err = math.log2(oracle.sq_weight(float(y), k)) - float(y) / 2 ** k
+        assert lo - 1e-12 <= err <= hi + 1e-12
+    # the finer rounding shrinks the worst error below Rowmax-H15's 0.335
+    assert hi < math.log2(1.5) - 0.25
+
+
+@pytest.mark.parametrize("k", [2, 3])
+def test_weights_exact_in_both_storage_types(k):
+    # at most k = 3 mantissa bits: every weight from 2^-6 up to the FP8
+    # anchor weight 2^8 is an e4m3 value, and every weight is a bf16 value
+    ws = [2.0 ** a * (1 + f / 2 ** k) for a in range(-6, 8) for f in range(2 ** k)] + [256.0]
+    for w in ws:
+        assert oracle.e4m3_value(oracle.e4m3_encode(w)) == w
+        b = int(np.array([w], np.float32).view(np.uint32)[0])
+        assert b & 0xFFFF == 0
+
+
+# ---- attention with the S(Q_{2^-k}) weight (per-tile running max) ---------
+
+from fractions import Fraction  # noqa: E402
+
+from test_oracle_attn import SCALE_C1_ONE, dequant, integer_inputs, round_f32, sdpa  # noqa: E402
+from paper_2609_33586_amd import synth  # noqa: E402
+
+BF16, FP8 = oracle.BF16, oracle.FP8_E4M3
+SQ_MODES = [(oracle.SQ4_TILE, 2), (oracle.SQ8_TILE, 3)]
+
+
+def sq_fraction(y: Fraction, k: int) -> Fraction:
+    """S(Q_{2^-k}(x)) in exact arithmetic on y = 2^k x, clamped at -126 * 2^k."""
+    y = max(y, Fraction(-126 * 2 ** k))
+    q = Fraction(round(y), 2 ** k)  # Python rounds a Fraction half to even
+    fl = math.floor(q)
+    return Fraction(2) ** fl * (1 + q - fl)
+
+
+@pytest.mark.parametrize("mode,k", SQ_MODES)
+@pytest.mark.parametrize("causal", [False, True])
+def test_sq_equals_softmax_when_differences_are_whole_octaves(mode, k, causal):
+    # c1 = 1 and integer logits: every x is an integer and S(x) = 2^x exactly
+    rng = np.random.default_rng(21)
+    inp = integer_inputs(1, 4, 2, 45, 4, rng)
+    o, lse = oracle.attn(inp.q, inp.k, inp.v, dtype=BF16, causal=causal, scale=SCALE_C1_ONE, mode=mode, Bc=8)
+    o_ref, lse_ref = sdpa(inp, causal, SCALE_C1_ONE)
+    assert np.max(np.abs(o - o_ref)) < 1e-12
+    assert np.max(np.abs(lse - lse_ref)) < 1e-12
+
+
+@pytest.mark.parametrize("mode,k", SQ_MODES)
+def test_sq_fp8_offset_cancels_for_whole_octaves(mode, k):
+    rng = np.random.default_rng(22)
+    q = rng.integers(-1, 2, (1, 2, 32, 4)).astype(np.float32)
+    kk = rng.integers(-1, 2, (1, 2, 32, 4)).astype(np.float32)
+    v = rng.integers(-3, 4, (1, 2, 32, 4)).astype(np.float32)
+    inp = synth.Inputs(synth.e4m3_codes(q), synth.e4m3_codes(kk), synth.e4m3_codes(v), (1.0, 1.0, 1.0), FP8)
+    o, lse = oracle.attn(inp.q, inp.k, inp.v, dtype=FP8, causal=True, scale=SCALE_C1_ONE, mode=mode, Bc=8)
+    o_ref, lse_ref = sdpa(inp, True, SCALE_C1_ONE)
+    assert np.max(np.abs(o - o_ref)) < 1e-12
+    assert np.max(np.abs(lse - lse_ref)) < 1e-12
+
+
+def sq_prefix_max_form(s, v, jend, c1, Bc, off, k):
+    """O and LSE of one row without the online recurrence: key j in tile t(j)
+    is weighted by S(Q_{2^-k}) of its exponent relative to the prefix max of
+    the tiles up to its own, times 2^(c1 (M_t(j) - M_final))."""
+    ck = np.float32(2.0 ** k) * c1
+    tiles = [(t0, min(t0 + Bc, jend)) for t0 in range(0, jend, Bc)]
+    prefix, m = [], -np.inf
+    for t0, t1 in tiles:
+        m = max(m, float(np.max(s[t0:t1])))
+        prefix.append(np.float32(m))
+    M = float(prefix[-1])
+    num, den = np.zeros(v.shape[1]), 0.0
+    for (t0, t1), Mt in zip(tiles, prefix):
+        nb = round_f32(-Fraction(float(Mt)) * Fraction(float(ck)) + 2 ** k * off)
+        for j in range(t0, t1):
+            y = round_f32(Fraction(float(s[j])) * Fraction(float(ck)) + Fraction(float(nb)))
+            w = float(sq_fraction(Fraction(float(y)), k)) * 2.0 ** (float(c1) * (float(Mt) - M))
+            num += w * v[j]
+            den += w
+    return num / den, math.log(2) * (M * float(c1) + math.log2(den) - off)
+
+
+@pytest.mark.parametrize("mode,k", SQ_MODES)
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("Bc", [1, 7, 16, 1000])
+def test_sq_tile_recurrence_matches_prefix_max_form(mode, k, causal, Bc):
+    inp = synth.make_inputs(1, 2, 2, 41, 8, BF16, sharp=True, seed=23)
+    scale = 0.9
+    o, lse = oracle.attn(inp.q, inp.k, inp.v, dtype=BF16, causal=causal, scale=scale, mode=mode, Bc=Bc)
+    c1 = np.float32(oracle.c1(scale))
+    _, _, vdq = dequant(inp)
+    for h in range(2):
+        for i in (0, 6, 7, 26, 40):
+            s = oracle.logits_row(inp.q, inp.k, BF16, 0, h, i)
+            jend = i + 1 if causal else 41
+            o_ref, lse_ref = sq_prefix_max_form(s, vdq[0, h], jend, c1, Bc, 0, k)
+            assert np.max(np.abs(o[0, h, i] - o_ref)) < 1e-12
+            assert abs(lse[0, h, i] - lse_ref) < 1e-12
+
+
+@pytest.mark.parametrize("mode,k", SQ_MODES)
+def test_sq_brute_force_tiny_with_fractions(mode, k):
+    # S=4, d=2, c1 = 1, one tile: logits on the quarter lattice, so each
+    # weight is S of an exact lattice point (k = 2) or its RNE neighbour
+    q = np.array([[1.0, 0.0], [0.0, 1.0], [0.5, 0.25], [2.0, -1.0]], np.float32)
+    kk = np.array([[0.25, 0.0], [1.5, 0.75], [-1.0, 2.5], [3.0, 0.5]], np.float32)
+    v = np.array([[1.0, -1.0], [2.0, 0.0], [3.0, 4.0], [4.0, 2.0]], np.float32)
+    inp = synth.Inputs(synth.bf16_bits(q[None, None]), synth.bf16_bits(kk[None, None]),
+                       synth.bf16_bits(v[None, None]), (1.0, 1.0, 1.0), BF16)
+    o, lse = oracle.attn(inp.q, inp.k, inp.v, dtype=BF16, causal=False, scale=SCALE_C1_ONE, mode=mode, Bc=4)
+    for i in range(4):
+        s = [Fraction(float(q[i] @ kk[j])) for j in range(4)]
+        m = max(s)
+        w = [sq_fraction(2 ** k * (sj - m), k) for sj in s]
+        den = sum(w)
+        for c in range(2):
+            num = sum(wj * Fraction(float(v[j, c])) for j, wj in enumerate(w))
+            assert abs(o[0, 0, i, c] - float(num / den)) < 1e-14
+        assert abs(lse[0, 0, i] - math.log(2) * (float(m) + math.log2(float(den)))) < 1e-14
+
+
+@pytest.mark.parametrize("k", [1, 2, 3])
+def test_row_from_logits_matches_weight_function(k):
+    # the per-row entry used against the GPU probe: W_j = S(Q_{2^-k}) of the
+    # exponent fma(s_j, 2^k c1, fma(-m, 2^k c1, 2^k off)) with m the row max (one tile)
+    rng = np.random.default_rng(24)
+    s = (rng.standard_normal(100) * 3).astype(np.float32)
+    c1 = np.float32(0.7)
+    for dtype, off in ((BF16, 0), (FP8, 8)):
+        w, p, _ = oracle.sq_row_from_logits(s, 99, False, float(c1), dtype, Bc=128, k=k)
+        ck = np.float32(2.0 ** k) * c1
+        m = np.float32(np.max(s))
+        nb = np.float32(round_f32(-Fraction(float(m)) * Fraction(float(ck)) + 2 ** k * off))
+        for j in range(100):
+            y = round_f32(Fraction(float(s[j])) * Fraction(float(ck)) + Fraction(float(nb)))
+            assert w[j] == np.float32(float(sq_fraction(Fraction(float(y)), k)))
