@@ -3,7 +3,8 @@
 One step = one attention forward (the whole hot path: QK^T, online softmax
 with the Rowmax-H15 weight, PV, epilogue) over the workload's synthetic
 inputs, already resident in HBM.  The exact-exp2 variant of the same kernel is
-timed the same way, in alternating rounds, as the control.
+timed the same way, in alternating rounds, as the control, and so are the
+finer input-rounding weights S(Q_{1/4}) and S(Q_{1/8}) (App. B.2).
 
 Prints ONE JSON line.  value = effective TFLOP/s of the H15 forward (FLOPs in
 the FlashAttention convention: 4 B Hq S^2 d, halved when causal).
@@ -37,7 +38,8 @@ def parse():
     ap.add_argument("--rounds", type=int, default=3)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU baseline sample time")
-    ap.add_argument("--modes", default="h15,exact")
+    ap.add_argument("--modes", default="h15,exact,sq4,sq8",
+                    help="weights to time: h15 (the method), exact (control), sq4/sq8 (S(Q_1/4), S(Q_1/8))")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="only run a plain device-to-device copy of this many GiB (5 times), "
                          "the reference for scaling HBM byte counters")
@@ -126,7 +128,7 @@ def main():
     out = torch.empty((w.B, w.Hq, w.S, w.d), dtype=torch.bfloat16, device=dev)
     lse = torch.empty((w.B, w.Hq, w.S), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
-    modes = {"h15": pkg.ATTN_EXP_H15, "exact": pkg.ATTN_EXP_EXACT}
+    modes = {"h15": pkg.ATTN_EXP_H15, "exact": pkg.ATTN_EXP_EXACT, "sq4": pkg.ATTN_EXP_SQ4, "sq8": pkg.ATTN_EXP_SQ8}
     want = [m for m in args.modes.split(",") if m in modes]
 
     def call(mode):
@@ -194,6 +196,14 @@ def main():
             "h15_vs_exact_speedup_pct": round(100.0 * (med["exact"] / med["h15"] - 1.0), 2),
             "windows_ms_per_call": {m: [round(t / n, 5) for t, n in windows[m]] for m in want},
         }
+    variants = [m for m in ("sq4", "sq8") if m in want]
+    if variants and "h15" in want:
+        # App. B.2's finer input rounding S(Q_{2^-k}), k = 2, 3: same kernel,
+        # timed in the same alternating rounds
+        med = {m: float(np.median([t / n for t, n in windows[m]])) for m in want}
+        line["input_rounding_variants"] = {
+            m: {"ms_per_call": round(res_ms[m], 5), "tflops": round(tflops[m], 2),
+                "vs_h15_pct": round(100.0 * (med["h15"] / med[m] - 1.0), 2)} for m in variants}
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(w, inp, scale, args.cpu_seconds)
     print(json.dumps(line), flush=True)

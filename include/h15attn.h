@@ -17,6 +17,16 @@
  *                   realised as y = fma(s, c2, fma(-m, c2, 2 off)),
  *                   y = max(y, -252), t = y + 0x1.8p23f (RNE),
  *                   w = bits^-1((bits(t) << 22) + bits(1.0f)), c2 = 2*c1.
+ *   ATTN_EXP_SQ4, ATTN_EXP_SQ8: the finer input rounding S(Q_{2^-k}(x)) for
+ *                   k = 2 and k = 3 (App. B.2 "Exponential-map ablation";
+ *                   Rowmax-H15 is k = 1): Q_{2^-k}(x) = 2^-k RNE(2^k x),
+ *                   S(q) = 2^floor(q) (1 + q - floor(q)) (App. B.1), realised
+ *                   as the H15 sequence with 2^k in place of the doubling:
+ *                   y = fma(s, ck, fma(-m, ck, 2^k off)), ck = 2^k c1,
+ *                   y = max(y, -126 * 2^k), t = y + 0x1.8p23f (RNE),
+ *                   w = bits^-1((bits(t) << (23 - k)) + bits(1.0f)).
+ *                   Every weight has at most k mantissa bits, so P = w is
+ *                   exact in bf16, and in e4m3 from 2^-6 up.
  * where s_ij = sum_c q_ic k_jc is the raw logit of the stored operands (bf16
  * values, or e4m3 values without their descales) accumulated in fp32,
  * c1 = fp32(scale * q_descale * k_descale * log2(e)) (products in double,
@@ -24,7 +34,8 @@
  * e4m3), and m the running maximum of the raw logits, moved at every key
  * tile to the maximum so far (rescale threshold 0, App. B.2: per-tile
  * running max).  The row sum and the PV product consume the same weights:
- * l sums w in fp32; PV multiplies V by P = w stored as bf16 (exact for H15)
+ * l sums w in fp32; PV multiplies V by P = w stored as bf16 (exact for the
+ * approximate weights)
  * or e4m3 (round to nearest even).  Output:
  *     O = (sum_j P_j V_j) / l * v_descale, stored as bf16;
  *     LSE = ln2 * (m * c1 + log2(l) - off)   (natural log of the normaliser
@@ -57,7 +68,7 @@ extern "C" {
 #endif
 
 enum attn_dtype { ATTN_BF16 = 0, ATTN_FP8_E4M3 = 1 };
-enum attn_expmode { ATTN_EXP_EXACT = 0, ATTN_EXP_H15 = 1 };
+enum attn_expmode { ATTN_EXP_EXACT = 0, ATTN_EXP_H15 = 1, ATTN_EXP_SQ4 = 2, ATTN_EXP_SQ8 = 3 };
 enum attn_status {
     ATTN_OK = 0,
     ATTN_EINVAL = -1,      /* null pointer, non-positive size, Hq % Hkv != 0,

@@ -60,13 +60,18 @@ constexpr int BUF_DWORD3 = 0x00020000;
 constexpr int SG_MFMA = 0x008;
 constexpr int SG_DS_READ = 0x100;
 constexpr float H15_MAGIC = 12582912.0f;  // 0x4B400000 = 2^23 + 2^22
+constexpr uint32_t MAGIC_BITS = 0x4B400000u;
 constexpr uint32_t ONE_BITS = 0x3F800000u;
-// clamp at -252 done on the integer form: bits(y + magic) - (0x4B400000 - 252),
-// saturated at zero, is n + 252 clamped at 0 whenever y + magic >= 0
-constexpr uint32_t CLAMP_BASE = 0x4B400000u - 252u;
-constexpr uint32_t CLAMP_BIAS = 0x00800000u;  // bits(2^-126) = bits(1.0) - (252 << 22)
+// bits(2^-126) = bits(1.0) - (126 << 23): the bias of the integer-clamp form
+constexpr uint32_t CLAMP_BIAS = 0x00800000u;
 
+// Kernel weight modes.  0 is the exact-exp2 control.  The input-rounding
+// family S(Q_{2^-k}) (App. B.2; k = 1 is Rowmax-H15, App. B.1) takes mode
+// 2k - 1 with the clamp in floating point and 2k with the clamp on the
+// integer form (exact only when y + 0x1.8p23 >= 0 for every score).
 enum { MODE_EXACT = 0, MODE_H15 = 1, MODE_H15_FASTCLAMP = 2 };
+constexpr int mode_order(int mode) { return (mode + 1) / 2; }
+constexpr bool mode_intclamp(int mode) { return mode != MODE_EXACT && mode % 2 == 0; }
 
 struct Params {
   const uint8_t* q;
@@ -75,7 +80,7 @@ struct Params {
   uint16_t* o;
   float* lse;
   int B, Hq, Hkv, S, G;
-  float c1, c2, vd;
+  float c1, ck, vd;  // base-two logit scale; 2^k c1 for the weight; V descale
   int nqb;    // query blocks per head
   int remap;  // XCD-grouped workgroup order is valid for this shape
   // probe target (PROBE instantiations only)
@@ -136,22 +141,27 @@ __device__ __forceinline__ void map_block(const Params& p, int L, int& qb, int& 
   }
 }
 
-// Rowmax-H15 weight of one score (App. B.1): doubled exponent y, clamp at
-// -252, RNE add of 0x4B400000, left shift by 22, plus the bits of 1.0.
+// Weight of one score, S(Q_{2^-k}(x)) with k = mode_order(MODE) (App. B.1
+// "Implementation" for k = 1, App. B.2 "Exponential-map ablation" for k = 2,
+// 3): y = 2^k x = fma(s, 2^k c1, nb), clamp at -126 * 2^k, RNE add of
+// 0x4B400000 (n = RNE(y) lands in the low mantissa bits), left shift by
+// 23 - k (the low k bits of n become the top mantissa bits, the rest the
+// exponent), plus the bits of 1.0, all modulo 2^32.
 template <int MODE>
-__device__ __forceinline__ float h15_weight(float s, float c2, float nb2) {
-  const float y = __builtin_fmaf(s, c2, nb2);
-  if constexpr (MODE == MODE_H15_FASTCLAMP) {
+__device__ __forceinline__ float sq_weight(float s, float ck, float nbk) {
+  constexpr int K = mode_order(MODE);
+  const float y = __builtin_fmaf(s, ck, nbk);
+  if constexpr (mode_intclamp(MODE)) {
     // Same bits as the canonical order when y + magic >= 0 (the launcher only
     // selects this form when every |y| is provably below 2^22): the clamp
-    // max(n, -252) is taken on n + 252 = bits(t) - CLAMP_BASE with unsigned
-    // saturation, and the bias of the final add absorbs the 252.
+    // max(n, -126 * 2^k) is taken on n + 126 * 2^k = bits(t) - base with
+    // unsigned saturation, and the bias of the final add absorbs the offset.
     const float t = y + H15_MAGIC;
-    const uint32_t n252 = __builtin_elementwise_sub_sat(__float_as_uint(t), CLAMP_BASE);
-    return __uint_as_float((n252 << 22) + CLAMP_BIAS);
+    const uint32_t nc = __builtin_elementwise_sub_sat(__float_as_uint(t), MAGIC_BITS - (126u << K));
+    return __uint_as_float((nc << (23 - K)) + CLAMP_BIAS);
   } else {
-    const float t = __builtin_fmaxf(y, -252.0f) + H15_MAGIC;
-    return __uint_as_float((__float_as_uint(t) << 22) + ONE_BITS);
+    const float t = __builtin_fmaxf(y, -126.0f * (float)(1 << K)) + H15_MAGIC;
+    return __uint_as_float((__float_as_uint(t) << (23 - K)) + ONE_BITS);
   }
 }
 
@@ -525,11 +535,11 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
 
     // weights, in place over the scores
     if constexpr (MODE != MODE_EXACT) {
-      const float nb2 = __builtin_fmaf(-m_new, p.c2, 2.0f * off);
+      const float nbk = __builtin_fmaf(-m_new, p.ck, (float)(1 << mode_order(MODE)) * off);
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int j = 0; j < 16; ++j) sacc[kb][j] = h15_weight<MODE>(sacc[kb][j], p.c2, nb2);
+        for (int j = 0; j < 16; ++j) sacc[kb][j] = sq_weight<MODE>(sacc[kb][j], p.ck, nbk);
       if (need_mask) {
         // masked keys carry weight 0 (the clamp alone would give 2^-126)
         const int lim = (CAUSAL ? min(qrow, S - 1) : S - 1) - kt0 - 4 * g;
@@ -665,20 +675,30 @@ hipError_t launch_one(const Params& p, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int DT, int D, bool PROBE>
-hipError_t launch_dt_d(const Params& p, int causal, int mode, hipStream_t st) {
-  if (causal) {
+template <int DT, int D, bool CAUSAL, bool PROBE>
+hipError_t launch_mode(const Params& p, int mode, hipStream_t st) {
+  switch (mode) {
+    case MODE_EXACT: return launch_one<DT, D, CAUSAL, MODE_EXACT, PROBE>(p, st);
+    case 1: return launch_one<DT, D, CAUSAL, 1, PROBE>(p, st);
+    case 3: return launch_one<DT, D, CAUSAL, 3, PROBE>(p, st);
+    case 5: return launch_one<DT, D, CAUSAL, 5, PROBE>(p, st);
+    default: break;
+  }
+  // the integer-clamp forms are only ever chosen for FP8
+  if constexpr (DT == DT_FP8) {
     switch (mode) {
-      case MODE_H15: return launch_one<DT, D, true, MODE_H15, PROBE>(p, st);
-      case MODE_H15_FASTCLAMP: return launch_one<DT, D, true, MODE_H15_FASTCLAMP, PROBE>(p, st);
-      default: return launch_one<DT, D, true, MODE_EXACT, PROBE>(p, st);
+      case 2: return launch_one<DT, D, CAUSAL, 2, PROBE>(p, st);
+      case 4: return launch_one<DT, D, CAUSAL, 4, PROBE>(p, st);
+      case 6: return launch_one<DT, D, CAUSAL, 6, PROBE>(p, st);
+      default: break;
     }
   }
-  switch (mode) {
-    case MODE_H15: return launch_one<DT, D, false, MODE_H15, PROBE>(p, st);
-    case MODE_H15_FASTCLAMP: return launch_one<DT, D, false, MODE_H15_FASTCLAMP, PROBE>(p, st);
-    default: return launch_one<DT, D, false, MODE_EXACT, PROBE>(p, st);
-  }
+  return hipErrorInvalidValue;
+}
+
+template <int DT, int D, bool PROBE>
+hipError_t launch_dt_d(const Params& p, int causal, int mode, hipStream_t st) {
+  return causal ? launch_mode<DT, D, true, PROBE>(p, mode, st) : launch_mode<DT, D, false, PROBE>(p, mode, st);
 }
 
 template <bool PROBE>
@@ -692,17 +712,28 @@ hipError_t launch_any(const Params& p, int dtype, int d, int causal, int mode, h
 
 bool finite_pos(float x) { return x > 0.0f && x < INFINITY; }
 
-// Kernel variant for an ABI exp_mode.  For FP8 every raw logit satisfies
-// |s| <= d * 448^2, so |y| <= 2 c2 d 448^2 + 16; when that is below 2^22 the
-// H15 exponent y + 0x1.8p23 can never go negative and the integer form of the
-// -252 clamp gives exactly the canonical bits.
-int kernel_mode(int dtype, int exp_mode, int d, float c2) {
-  if (exp_mode == ATTN_EXP_EXACT) return MODE_EXACT;
-  if (dtype == ATTN_FP8_E4M3) {
-    const double ymax = 2.0 * (double)c2 * (double)d * 448.0 * 448.0 * (1.0 + 1e-5) + 16.0;
-    if (ymax < 4194304.0) return MODE_H15_FASTCLAMP;
+// Input-rounding order k of an ABI exp_mode (0 for the exact control).
+int exp_order(int exp_mode) {
+  switch (exp_mode) {
+    case ATTN_EXP_H15: return 1;
+    case ATTN_EXP_SQ4: return 2;
+    case ATTN_EXP_SQ8: return 3;
+    default: return 0;
   }
-  return MODE_H15;
+}
+
+// Kernel variant for an ABI exp_mode.  For FP8 every raw logit satisfies
+// |s| <= d * 448^2, so |y| <= 2 ck d 448^2 + 8 * 2^k with ck = 2^k c1; when
+// that is below 2^22 the exponent y + 0x1.8p23 can never go negative and the
+// integer form of the clamp gives exactly the canonical bits.
+int kernel_mode(int dtype, int exp_mode, int d, float ck) {
+  const int k = exp_order(exp_mode);
+  if (k == 0) return MODE_EXACT;
+  if (dtype == ATTN_FP8_E4M3) {
+    const double ymax = 2.0 * (double)ck * (double)d * 448.0 * 448.0 * (1.0 + 1e-5) + 8.0 * (1 << k);
+    if (ymax < 4194304.0) return 2 * k;
+  }
+  return 2 * k - 1;
 }
 
 // query rows per workgroup for an operand type
@@ -718,7 +749,7 @@ int fill_params(Params& p, const void* q, const void* k, const void* v, void* o,
   if (Hq % Hkv != 0) return ATTN_EINVAL;
   if (!finite_pos(scale)) return ATTN_EINVAL;
   if (dtype != ATTN_BF16 && dtype != ATTN_FP8_E4M3) return ATTN_EUNSUPPORTED;
-  if (exp_mode != ATTN_EXP_EXACT && exp_mode != ATTN_EXP_H15) return ATTN_EUNSUPPORTED;
+  if (exp_mode != ATTN_EXP_EXACT && exp_order(exp_mode) == 0) return ATTN_EUNSUPPORTED;
   if (d != 64 && d != 128) return ATTN_EUNSUPPORTED;
   const uintptr_t mis = (uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)o;
   if (mis & 15u) return ATTN_EUNSUPPORTED;
@@ -746,10 +777,11 @@ int fill_params(Params& p, const void* q, const void* k, const void* v, void* o,
   p.Hkv = Hkv;
   p.S = S;
   p.G = Hq / Hkv;
-  // base-two exponent scale of a raw logit; the H15 path uses the doubled
-  // constant (App. B.1), the rescale factor and LSE the plain one
+  // base-two exponent scale of a raw logit; the weight uses 2^k times it
+  // (the doubled constant of App. B.1 for k = 1; the scaling is exact), the
+  // rescale factor and LSE the plain one
   p.c1 = (float)((double)scale * (double)qd * (double)kd * 1.4426950408889634);
-  p.c2 = 2.0f * p.c1;
+  p.ck = ldexpf(p.c1, exp_order(exp_mode));
   p.vd = vd;
   p.nqb = (S + row_block(dtype) - 1) / row_block(dtype);
   p.remap = ((B * Hkv) % 8 == 0) ? 1 : 0;
@@ -779,7 +811,7 @@ int attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse
   const int rc = fill_params(p, q, k, v, o, lse, B, Hq, Hkv, S, d, scale, dtype, exp_mode, opts);
   if (rc != ATTN_OK) return rc;
   hipStream_t st = opts ? (hipStream_t)opts->stream : nullptr;
-  const int mode = kernel_mode(dtype, exp_mode, d, p.c2);
+  const int mode = kernel_mode(dtype, exp_mode, d, p.ck);
   const hipError_t e = launch_any<false>(p, dtype, d, causal ? 1 : 0, mode, st);
   return e == hipSuccess ? ATTN_OK : ATTN_ELAUNCH;
 }
@@ -811,7 +843,7 @@ int attn_fwd_probe(const void* q, const void* k, const void* v, void* o, float* 
   hipLaunchKernelGGL(probe_fill, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, s_out, w_out,
                      p_bits_out, n);
   if (hipGetLastError() != hipSuccess) return ATTN_ELAUNCH;
-  const int mode = kernel_mode(dtype, exp_mode, d, p.c2);
+  const int mode = kernel_mode(dtype, exp_mode, d, p.ck);
   const hipError_t e = launch_any<true>(p, dtype, d, causal ? 1 : 0, mode, st);
   return e == hipSuccess ? ATTN_OK : ATTN_ELAUNCH;
 }

@@ -9,7 +9,8 @@ and every row to 5e-2 (a weight on the other side of an RNE boundary, caused
 by the fp32 accumulation order of the logit, moves LSE by a fraction of that
 weight), and against the oracle fed the GPU's own logits to 1e-5.  The H15
 weights and stored P are compared bit for bit when the oracle is fed the
-GPU's own fp32 logits."""
+GPU's own fp32 logits.  The finer input-rounding weights S(Q_{2^-k}) for
+k = 2, 3 (exp modes SQ4, SQ8) are held to the same bars as H15."""
 import math
 import sys
 
@@ -24,7 +25,11 @@ from paper_2609_33586_amd import synth
 pytestmark = pytest.mark.gpu
 
 BF16, FP8 = synth.BF16, synth.FP8_E4M3
-EXACT, H15 = pkg.ATTN_EXP_EXACT, pkg.ATTN_EXP_H15
+EXACT, H15, SQ4, SQ8 = pkg.ATTN_EXP_EXACT, pkg.ATTN_EXP_H15, pkg.ATTN_EXP_SQ4, pkg.ATTN_EXP_SQ8
+APPROX = (H15, SQ4, SQ8)
+ALL_MODES = (EXACT,) + APPROX
+ORACLE_MODE = {EXACT: oracle.EXACT, H15: oracle.H15_TILE, SQ4: oracle.SQ4_TILE, SQ8: oracle.SQ8_TILE}
+ORDER = {H15: 1, SQ4: 2, SQ8: 3}  # input-rounding exponent k
 TOL = {BF16: 2e-2, FP8: 6e-2}
 LSE_TOL = 1e-3
 LSE_TOL_H15 = 5e-2
@@ -59,7 +64,7 @@ def gpu_run(inp, causal, scale, mode, tensors=None):
 
 
 def oracle_run(inp, causal, scale, mode, rows=None):
-    om = oracle.EXACT if mode == EXACT else oracle.H15_TILE
+    om = ORACLE_MODE[mode]
     return oracle.attn(inp.q, inp.k, inp.v, dtype=inp.dtype, causal=causal, scale=scale, mode=om,
                        descale=inp.descale, Bc=pkg.attn_tile_bc(), rows=rows)
 
@@ -73,7 +78,7 @@ def assert_close(inp, o, lse, o_ref, lse_ref, what, mode=EXACT):
         f"rows |dLSE|>1e-4: {np.mean(dl > 1e-4):.4f}")
     assert np.all(np.isfinite(o)) and np.all(np.isfinite(lse))
     assert err <= bound, what
-    if mode == H15:
+    if mode in APPROX:
         # Against the oracle's own logits, a few weights sit on the other side
         # of an RNE boundary (fp32 accumulation order of the logits), which
         # moves LSE by a fraction of one weight; the exact LSE check is the
@@ -87,7 +92,7 @@ SMALL = [(dt, d, causal, S) for dt in (BF16, FP8) for d in (64, 128) for causal 
          for S in (256, 300)]
 
 
-@pytest.mark.parametrize("mode", [EXACT, H15])
+@pytest.mark.parametrize("mode", ALL_MODES)
 @pytest.mark.parametrize("dt,d,causal,S", SMALL)
 def test_small_full_parity(dt, d, causal, S, mode):
     inp = synth.make_inputs(1, 4, 2, S, d, dt, sharp=True, seed=100 + S + d)
@@ -98,16 +103,13 @@ def test_small_full_parity(dt, d, causal, S, mode):
     assert_close(inp, o, lse, o_ref.reshape(o.shape), lse_ref.reshape(lse.shape), "full", mode)
 
 
-@pytest.mark.parametrize("dt", [BF16, FP8])
-@pytest.mark.parametrize("causal", [False, True])
-@pytest.mark.parametrize("mode", [EXACT, H15])
-def test_probe_weights_bit_exact(dt, causal, mode):
-    S, d = 520, 128
-    inp = synth.make_inputs(1, 4, 1, S, d, dt, sharp=True, seed=201)
-    sc = scale_of(d)
+def check_probe(inp, S, d, dt, causal, mode, sc, rowsets):
+    """Probe rows of the kernel: logits close to the exact dot products, and W,
+    P and LSE bit-identical (to 1e-5 for LSE) to the oracle fed those logits."""
     q, k, v = dev_tensors(inp)
     c1 = oracle.c1(sc, inp.descale[0], inp.descale[1])
-    for (b, h, r0, n) in ((0, 0, 0, 40), (0, 3, 250, 40), (0, 2, S - 37, 37)):
+    G = inp.q.shape[1] // inp.k.shape[1]
+    for (b, h, r0, n) in rowsets:
         say(f"probe dtype={dt} causal={causal} mode={mode} rows {r0}+{n} head {h}")
         o_p, lse_p, s, w, pbits = pkg.attn_fwd_probe(q, k, v, causal=causal, scale=sc, exp_mode=mode,
                                                      b=b, h=h, row0=r0, nrows=n, descale=inp.descale)
@@ -120,7 +122,7 @@ def test_probe_weights_bit_exact(dt, causal, mode):
         lse_p = lse_p.cpu().numpy()
         dec = synth.bf16_decode if dt == BF16 else synth.e4m3_decode
         qv = np.asarray(dec(inp.q[b, h]), np.float64)
-        kv = np.asarray(dec(inp.k[b, h // 4]), np.float64)
+        kv = np.asarray(dec(inp.k[b, h // G]), np.float64)
         for r in range(n):
             i = r0 + r
             jend = i + 1 if causal else S
@@ -135,11 +137,14 @@ def test_probe_weights_bit_exact(dt, causal, mode):
             if r == 0:
                 say(f"  logit error / sum|q k|: {rel:.3e}")
             assert rel <= (2.0 ** -16 if dt == BF16 else 2.0 ** -12)
-            w_ref, p_ref, lse_ref = oracle.h15_row_from_logits(s[r], i, causal, c1, dt, pkg.attn_tile_bc(),
-                                                               exact_exp=(mode == EXACT))
-            if mode == H15:
+            if mode in APPROX:
+                w_ref, p_ref, lse_ref = oracle.sq_row_from_logits(s[r], i, causal, c1, dt, pkg.attn_tile_bc(),
+                                                                  k=ORDER[mode])
+            else:
+                w_ref, p_ref, lse_ref = oracle.h15_row_from_logits(s[r], i, causal, c1, dt, pkg.attn_tile_bc(),
+                                                                   exact_exp=True)
+            if mode in APPROX:
                 assert abs(lse_p[b, h, i] - lse_ref) <= 1e-5, f"row {i}"
-            if mode == H15:
                 assert np.array_equal(w[r].view(np.uint32), w_ref.view(np.uint32)), f"row {i}"
                 assert np.array_equal(pbits[r], p_ref), f"row {i}"
             else:
@@ -150,6 +155,33 @@ def test_probe_weights_bit_exact(dt, causal, mode):
                                  ((int(np.array([x], np.float32).view(np.uint32)[0]) >> 16) & 1)) >> 16
                                 if dt == BF16 else oracle.e4m3_encode(float(x)) for x in w[r]], np.uint32)
                 assert np.array_equal(pbits[r], enc), f"row {i}"
+
+
+@pytest.mark.parametrize("dt", [BF16, FP8])
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("mode", ALL_MODES)
+def test_probe_weights_bit_exact(dt, causal, mode):
+    S, d = 520, 128
+    inp = synth.make_inputs(1, 4, 1, S, d, dt, sharp=True, seed=201)
+    check_probe(inp, S, d, dt, causal, mode, scale_of(d), ((0, 0, 0, 40), (0, 3, 250, 40), (0, 2, S - 37, 37)))
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("mode", APPROX)
+def test_fp8_unit_descales_float_clamp_path(causal, mode):
+    # With unit descales the FP8 exponent bound 2 * 2^k c1 d 448^2 exceeds
+    # 2^22, so the library takes the floating-point clamp form instead of the
+    # integer one: the same bits are required.
+    S, d = 300, 128
+    rng = np.random.default_rng(210)
+    x = [rng.integers(-3, 4, shape).astype(np.float32) for shape in ((1, 2, S, d), (1, 1, S, d), (1, 1, S, d))]
+    inp = synth.Inputs(*(synth.e4m3_codes(a) for a in x), (1.0, 1.0, 1.0), FP8)
+    sc = scale_of(d)
+    assert 2.0 * 2.0 ** ORDER[mode] * oracle.c1(sc) * d * 448.0 ** 2 > 2.0 ** 22
+    check_probe(inp, S, d, FP8, causal, mode, sc, ((0, 0, 0, 30), (0, 1, S - 30, 30)))
+    o, lse = gpu_run(inp, causal, sc, mode)
+    o_ref, lse_ref = oracle_run(inp, causal, sc, mode)
+    assert_close(inp, o, lse, o_ref, lse_ref, "unit descales", mode)
 
 
 @pytest.mark.parametrize("dt", [BF16, FP8])
@@ -185,8 +217,12 @@ def test_one_hot_value_gates(dt, S):
 WORKLOADS = list(synth.WORKLOADS.values())
 
 
-@pytest.mark.parametrize("mode", [EXACT, H15])
-@pytest.mark.parametrize("w", WORKLOADS, ids=[w.name for w in WORKLOADS])
+FULL_CASES = [(w, m) for w in WORKLOADS for m in (EXACT, H15)] + [
+    (synth.WORKLOADS[n], m) for n in ("causal_fp8_b2_h32kv8_s8192_d128_sharp", "causal_bf16_b4_h32kv8_s2048_d128_sharp")
+    for m in (SQ4, SQ8)]
+
+
+@pytest.mark.parametrize("w,mode", FULL_CASES, ids=[f"{w.name}-{m}" for w, m in FULL_CASES])
 def test_full_size_sampled_rows(w, mode):
     say(f"full-size {w.name} mode={mode}: generating inputs")
     inp = synth.workload_inputs(w)
@@ -206,20 +242,22 @@ def test_full_size_sampled_rows(w, mode):
     assert_close(inp, o.reshape(-1, w.d)[rows], lse.reshape(-1)[rows], o_ref, lse_ref, "sampled rows", mode)
 
 
+@pytest.mark.parametrize("mode", APPROX)
 @pytest.mark.parametrize("w", [x for x in WORKLOADS if x.S >= 8192], ids=lambda x: x.name)
-def test_full_size_probe_bit_exact(w):
+def test_full_size_probe_bit_exact(w, mode):
     inp = synth.workload_inputs(w)
     sc = scale_of(w.d)
     q, k, v = dev_tensors(inp)
     c1 = oracle.c1(sc, inp.descale[0], inp.descale[1])
     b, h, r0, n = w.B - 1, w.Hq - 1, w.S - 40, 40
-    say(f"full-size probe {w.name} rows {r0}+{n}")
-    _, _, s, wt, pbits = pkg.attn_fwd_probe(q, k, v, causal=w.causal, scale=sc, exp_mode=H15, b=b, h=h,
+    say(f"full-size probe {w.name} mode={mode} rows {r0}+{n}")
+    _, _, s, wt, pbits = pkg.attn_fwd_probe(q, k, v, causal=w.causal, scale=sc, exp_mode=mode, b=b, h=h,
                                             row0=r0, nrows=n, descale=inp.descale)
     torch.cuda.synchronize()
     s, wt, pbits = s.cpu().numpy(), wt.cpu().numpy(), pbits.cpu().numpy().astype(np.uint32)
     for r in range(0, n, 7):
-        w_ref, p_ref, _ = oracle.h15_row_from_logits(s[r], r0 + r, w.causal, c1, w.dtype, pkg.attn_tile_bc())
+        w_ref, p_ref, _ = oracle.sq_row_from_logits(s[r], r0 + r, w.causal, c1, w.dtype, pkg.attn_tile_bc(),
+                                                    k=ORDER[mode])
         assert np.array_equal(wt[r].view(np.uint32), w_ref.view(np.uint32))
         assert np.array_equal(pbits[r], p_ref)
 
@@ -251,7 +289,7 @@ def test_edge_shapes(B, Hq, Hkv, S, d, dt):
     inp = synth.make_inputs(B, Hq, Hkv, S, d, dt, sharp=False, seed=500 + S)
     sc = scale_of(d)
     for causal in (False, True):
-        for mode in (EXACT, H15):
+        for mode in ALL_MODES:
             say(f"edge B={B} Hq={Hq} Hkv={Hkv} S={S} d={d} dtype={dt} causal={causal} mode={mode}")
             o, lse = gpu_run(inp, causal, sc, mode)
             o_ref, lse_ref = oracle_run(inp, causal, sc, mode)
