@@ -68,7 +68,11 @@ def lib() -> ctypes.CDLL:
     L.oracle_h15_row_from_logits.argtypes = [c_p, c_i, c_i, c_i, c_f, c_i, c_i, c_d, c_i, c_p, c_p, c_p]
     L.oracle_h15_row_from_logits.restype = c_i
     L.oracle_attn.argtypes = [c_p, c_p, c_p, c_i, c_d, c_d, c_d, c_i, c_i, c_i, c_i, c_i, c_i, c_d,
-                              c_i, c_i, c_d, c_p, c_i64, c_p, c_p]
+                              c_i, c_i, c_d, c_i, c_p, c_i64, c_p, c_p]
+    L.oracle_group_moves_from_logits.argtypes = [c_p, c_i, c_i, c_i, c_i, c_f, c_i, c_d, c_p]
+    L.oracle_group_moves_from_logits.restype = c_i
+    L.oracle_sq_row_from_logits_moves.argtypes = [c_p, c_i, c_i, c_i, c_f, c_i, c_i, c_p, c_i, c_p, c_p, c_p]
+    L.oracle_sq_row_from_logits_moves.restype = c_i
     L.oracle_attn.restype = c_i
     L.oracle_logits_row.argtypes = [c_p, c_p, c_i, c_i, c_i, c_i, c_i, c_i, c_i, c_i, c_i, c_p]
     L.oracle_logits_row.restype = c_i
@@ -174,13 +178,45 @@ def sq_row_from_logits(s: np.ndarray, i: int, causal: bool, c1_: float, dtype: i
     return w, p, lse.value
 
 
+def group_moves_from_logits(s: np.ndarray, i0: int, causal: bool, c1_: float, Bc: int, tau: float) -> np.ndarray:
+    """Per-tile anchor decisions shared by the rows i0 .. i0 + len(s) - 1, from
+    their fp32 logits s [rows, S] (1: move every row's anchor to its max)."""
+    s = np.ascontiguousarray(s, dtype=np.float32)
+    n, S = s.shape
+    move = np.zeros(S // Bc + 1, np.uint8)
+    rc = lib().oracle_group_moves_from_logits(_ptr(s), S, int(i0), int(i0 + n), int(bool(causal)), float(c1_),
+                                              int(Bc), float(tau), _ptr(move))
+    if rc != 0:
+        raise ValueError("oracle_group_moves_from_logits: invalid arguments")
+    return move
+
+
+def sq_row_from_logits_moves(s: np.ndarray, i: int, causal: bool, c1_: float, dtype: int, Bc: int, k: int,
+                             move: np.ndarray):
+    """As sq_row_from_logits with the per-tile anchor decisions given."""
+    s = np.ascontiguousarray(s, dtype=np.float32)
+    move = np.ascontiguousarray(move, dtype=np.uint8)
+    S = s.shape[0]
+    w = np.zeros(S, np.float32)
+    p = np.zeros(S, np.uint32)
+    lse = ctypes.c_double(0.0)
+    rc = lib().oracle_sq_row_from_logits_moves(_ptr(s), S, int(i), int(bool(causal)), float(c1_), int(dtype),
+                                               int(Bc), _ptr(move), int(k), _ptr(w), _ptr(p), ctypes.byref(lse))
+    if rc != 0:
+        raise ValueError("oracle_sq_row_from_logits_moves: invalid arguments")
+    return w, p, lse.value
+
+
 def attn(q: np.ndarray, k: np.ndarray, v: np.ndarray, *, dtype: int, causal: bool, scale: float,
-         mode: int, descale=(1.0, 1.0, 1.0), Bc: int = 128, tau: float = 0.0,
+         mode: int, descale=(1.0, 1.0, 1.0), Bc: int = 128, tau: float = 0.0, tau_group: int = 1,
          rows: np.ndarray | None = None):
     """Attention forward on stored operands.
 
     q: [B,Hq,S,d], k/v: [B,Hkv,S,d]; uint16 bf16 bit patterns (dtype BF16) or
-    uint8 e4m3 codes (dtype FP8_E4M3).  rows: optional flat row indices
+    uint8 e4m3 codes (dtype FP8_E4M3).  tau: conditional-rescale threshold in
+    base-two units (0: the anchor is always the running max); tau_group: rows
+    per shared anchor decision (1: per row; 32: per aligned group of 32 rows,
+    as FlashAttention-4 decides per warp).  rows: optional flat row indices
     (b*Hq + h)*S + i.  Returns (O [nrows, d] float64, LSE [nrows] float64);
     without rows the shapes are [B,Hq,S,d] and [B,Hq,S]."""
     want = np.uint16 if dtype == BF16 else np.uint8
@@ -201,7 +237,7 @@ def attn(q: np.ndarray, k: np.ndarray, v: np.ndarray, *, dtype: int, causal: boo
     lse = np.zeros(nrows, np.float64)
     qd, kd, vd = (float(x) for x in descale)
     rc = lib().oracle_attn(_ptr(q), _ptr(k), _ptr(v), int(dtype), qd, kd, vd, B, Hq, Hkv, S, d,
-                           int(bool(causal)), float(scale), int(mode), int(Bc), float(tau),
+                           int(bool(causal)), float(scale), int(mode), int(Bc), float(tau), int(tau_group),
                            _ptr(rows_arr), int(nrows), _ptr(o), _ptr(lse))
     if rc != 0:
         raise ValueError("oracle_attn: invalid arguments")

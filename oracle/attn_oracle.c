@@ -259,9 +259,25 @@ float oracle_c1(double scale, double qd, double kd)
  *   vrows  decoded V rows [S][d] (NULL: no O accumulation)
  *   jend   number of valid keys (keys 0 .. jend-1), >= 1
  * Outputs (each optional): o[d] (unscaled by vd), *lse, w[S], p[S]. */
+/* The anchor rule of App. B.2 "Conditional rescaling moves the anchor": the
+ * running max moves to max(m, mt) only when it grows by more than tau in
+ * base-two units, (mt - m) c1 > tau, evaluated in FP32 like the rest of the
+ * exponent path; with tau = 0 this is always max(m, mt).  The first tile with
+ * a valid key always sets the anchor. */
+static int grows(float mt, float m, float c1, double tau)
+{
+    if (m == -INFINITY) return 1;
+    volatile float dm = mt - m;
+    volatile float g = dm * c1;
+    return g > (float)tau;
+}
+
+/*   move   optional per-tile decisions (1: move the anchor to max(m, mt)),
+ *          used for a decision shared by a group of rows; NULL: this row's
+ *          own test with tau. */
 static void tiled_row(const float* s, const double* vrows, int S, int d, int jend, float c1,
-                      int off, int Bc, double tau, int dtype, int exact_exp, int kq, double vd,
-                      double* o, double* lse, float* w, uint32_t* p, double* acc)
+                      int off, int Bc, double tau, const uint8_t* move, int dtype, int exact_exp,
+                      int kq, double vd, double* o, double* lse, float* w, uint32_t* p, double* acc)
 {
     /* the input-rounding exponent k: 1 for Rowmax-H15 (c2 = 2 c1, shift 22),
      * 2 or 3 for S(Q_{2^-k}) (2^k c1, shift 23 - k); the scaling by 2^k is exact */
@@ -278,9 +294,8 @@ static void tiled_row(const float* s, const double* vrows, int S, int d, int jen
         int v1 = t1 < jend ? t1 : jend;
         float mt = -INFINITY;
         for (int j = t0; j < v1; j++) mt = fmaxf(mt, s[j]);
-        float m_new;
-        if (m == -INFINITY) m_new = mt;
-        else m_new = (((double)mt - (double)m) * (double)c1 > tau) ? fmaxf(m, mt) : m;
+        int mv = move ? (m == -INFINITY || move[t0 / Bc]) : grows(mt, m, c1, tau);
+        float m_new = mv ? fmaxf(m, mt) : m;
         double alpha = (m == -INFINITY) ? 0.0 : exp2(((double)m - (double)m_new) * (double)c1);
         l *= alpha;
         if (acc) for (int c = 0; c < d; c++) acc[c] *= alpha;
@@ -322,7 +337,21 @@ int oracle_sq_row_from_logits(const float* s, int S, int i, int causal, float c1
     if (S <= 0 || Bc <= 0 || i < 0 || i >= S || k < 1 || k > 3) return -1;
     int off = dtype == OR_FP8_E4M3 ? 8 : 0;
     int jend = causal ? i + 1 : S;
-    tiled_row(s, NULL, S, 0, jend, c1, off, Bc, tau, dtype, exact_exp, k, 1.0, NULL, lse_out, w_out,
+    tiled_row(s, NULL, S, 0, jend, c1, off, Bc, tau, NULL, dtype, exact_exp, k, 1.0, NULL, lse_out, w_out,
+              p_out, NULL);
+    return 0;
+}
+
+/* As oracle_sq_row_from_logits with the per-tile anchor decisions given
+ * (move[t] for tile t), for rows that share a group decision. */
+int oracle_sq_row_from_logits_moves(const float* s, int S, int i, int causal, float c1, int dtype,
+                                    int Bc, const uint8_t* move, int k, float* w_out,
+                                    uint32_t* p_out, double* lse_out)
+{
+    if (S <= 0 || Bc <= 0 || i < 0 || i >= S || k < 1 || k > 3 || !move) return -1;
+    int off = dtype == OR_FP8_E4M3 ? 8 : 0;
+    int jend = causal ? i + 1 : S;
+    tiled_row(s, NULL, S, 0, jend, c1, off, Bc, 0.0, move, dtype, 0, k, 1.0, NULL, lse_out, w_out,
               p_out, NULL);
     return 0;
 }
@@ -333,6 +362,62 @@ int oracle_h15_row_from_logits(const float* s, int S, int i, int causal, float c
 {
     return oracle_sq_row_from_logits(s, S, i, causal, c1, dtype, Bc, tau, exact_exp, 1, w_out,
                                      p_out, lse_out);
+}
+
+/* ---- the anchor decision shared by a group of rows ---------------------- */
+
+static double decode(const void* base, size_t idx, int dtype);
+
+/* FlashAttention-4 takes the conditional-rescale decision per warp of 32
+ * query rows (App. B.2, "Semantic simulation": the simulation decides per
+ * row, the kernel per warp of 32 rows): every row of the group moves its
+ * anchor to max(m, mt) when any row's anchor grows by more than tau.  The
+ * per-tile decisions (move[t] for tile t) of rows [i0, i1) from their fp32
+ * logits (row r of the group at s + r * S). */
+int oracle_group_moves_from_logits(const float* s, int S, int i0, int i1, int causal, float c1,
+                                   int Bc, double tau, uint8_t* move)
+{
+    if (S <= 0 || Bc <= 0 || i0 < 0 || i1 <= i0 || i1 > S || !move) return -1;
+    const int n = i1 - i0;
+    float m[n];
+    for (int r = 0; r < n; r++) m[r] = -INFINITY;
+    for (int t = 0; t * Bc < S; t++) {
+        int any = 0;
+        float mt[n];
+        for (int r = 0; r < n; r++) {
+            const int jend = causal ? i0 + r + 1 : S;
+            const int t0 = t * Bc, t1 = (t0 + Bc < jend) ? t0 + Bc : jend;
+            mt[r] = -INFINITY;
+            for (int j = t0; j < t1; j++) mt[r] = fmaxf(mt[r], s[(size_t)r * S + j]);
+            if (mt[r] != -INFINITY && grows(mt[r], m[r], c1, tau)) any = 1;
+        }
+        move[t] = (uint8_t)any;
+        for (int r = 0; r < n; r++)
+            if (m[r] == -INFINITY || any) m[r] = fmaxf(m[r], mt[r]);
+    }
+    return 0;
+}
+
+/* The same decisions for rows [i0, i1) of head (b, h) of stored operands. */
+static void group_moves(const void* q, const void* k, int dtype, int Hq, int Hkv, int S, int d,
+                        int b, int h, int i0, int i1, int causal, float c1, int Bc, double tau,
+                        uint8_t* move)
+{
+    const int n = i1 - i0, hk = h / (Hq / Hkv);
+    const size_t kvoff = ((size_t)b * Hkv + hk) * S * d;
+    float* s32 = malloc(sizeof(float) * (size_t)n * S);
+    double* qrow = malloc(sizeof(double) * d);
+    for (int r = 0; r < n; r++) {
+        const size_t qoff = (((size_t)b * Hq + h) * S + i0 + r) * d;
+        for (int c = 0; c < d; c++) qrow[c] = decode(q, qoff + c, dtype);
+        for (int j = 0; j < S; j++) {
+            double dot = 0.0;
+            for (int c = 0; c < d; c++) dot += qrow[c] * decode(k, kvoff + (size_t)j * d + c, dtype);
+            s32[(size_t)r * S + j] = (float)dot;
+        }
+    }
+    oracle_group_moves_from_logits(s32, S, i0, i1, causal, c1, Bc, tau, move);
+    free(s32); free(qrow);
 }
 
 /* ---- full attention --------------------------------------------------- */
@@ -352,8 +437,10 @@ static double decode(const void* base, size_t idx, int dtype)
  * Returns 0, or -1 on invalid arguments. */
 int oracle_attn(const void* q, const void* k, const void* v, int dtype, double qd, double kd,
                 double vd, int B, int Hq, int Hkv, int S, int d, int causal, double scale, int mode,
-                int Bc, double tau, const int64_t* rows, int64_t nrows, double* o, double* lse)
+                int Bc, double tau, int tau_group, const int64_t* rows, int64_t nrows, double* o,
+                double* lse)
 {
+    if (tau_group < 1) return -1;
     if (!q || !k || !v || !o || B <= 0 || Hq <= 0 || Hkv <= 0 || S <= 0 || d <= 0) return -1;
     if (Hq % Hkv != 0 || (dtype != OR_BF16 && dtype != OR_FP8_E4M3) || mode < 0 || mode > 6)
         return -1;
@@ -416,8 +503,16 @@ int oracle_attn(const void* q, const void* k, const void* v, int dtype, double q
         } else {
             int tile = (mode == OR_H15_WHOLEROW) ? S : Bc;
             int kq = mode == OR_SQ4_TILE ? 2 : mode == OR_SQ8_TILE ? 3 : 1;
-            tiled_row(s32, vrows, S, d, jend, c1, off, tile, tau, dtype, mode == OR_EXACT_TILE, kq,
+            uint8_t* move = NULL;
+            if (tau_group > 1) {
+                const int i0 = i / tau_group * tau_group;
+                const int i1 = i0 + tau_group < S ? i0 + tau_group : S;
+                move = malloc((size_t)(S / tile + 1));
+                group_moves(q, k, dtype, Hq, Hkv, S, d, b, h, i0, i1, causal, c1, tile, tau, move);
+            }
+            tiled_row(s32, vrows, S, d, jend, c1, off, tile, tau, move, dtype, mode == OR_EXACT_TILE, kq,
                       vd, orow, lse ? &lse[r] : NULL, NULL, NULL, acc);
+            free(move);
         }
         free(qrow); free(sexact); free(vrows); free(acc); free(s32);
     }
