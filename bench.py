@@ -40,6 +40,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU baseline sample time")
     ap.add_argument("--modes", default="h15,exact,sq4,sq8",
                     help="weights to time: h15 (the method), exact (control), sq4/sq8 (S(Q_1/4), S(Q_1/8))")
+    ap.add_argument("--tau", type=float, default=0.0,
+                    help="conditional-rescale threshold in octaves (BF16 workloads only; 0 = running max)")
+    ap.add_argument("--tau-per-wave", action="store_true", help="share the rescale decision per 32-row wave")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="only run a plain device-to-device copy of this many GiB (5 times), "
                          "the reference for scaling HBM byte counters")
@@ -131,9 +134,13 @@ def main():
     modes = {"h15": pkg.ATTN_EXP_H15, "exact": pkg.ATTN_EXP_EXACT, "sq4": pkg.ATTN_EXP_SQ4, "sq8": pkg.ATTN_EXP_SQ8}
     want = [m for m in args.modes.split(",") if m in modes]
 
+    if args.tau != 0.0 and w.dtype != synth.BF16:
+        print("bench.py: --tau applies to BF16 workloads only (FP8 keeps the running max)", file=sys.stderr)
+        sys.exit(2)
+
     def call(mode):
         pkg.attn_fwd_ex(q, k, v, causal=w.causal, scale=scale, exp_mode=modes[mode], descale=inp.descale,
-                        stream=stream, out=out, lse=lse)
+                        stream=stream, out=out, lse=lse, tau=args.tau, tau_per_wave=args.tau_per_wave)
 
     for mode in want:
         for _ in range(args.warmup):
@@ -183,7 +190,8 @@ def main():
         "dtype": dtname,
         "data": "synthetic (seeded Gaussian Q/K/V, 2% sharp keys where named)",
         "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "S": w.S, "d": w.d,
-                   "causal": w.causal, "exp_mode": head, "parallelism": "single GPU"},
+                   "causal": w.causal, "exp_mode": head, "rescale_threshold": args.tau,
+                   "rescale_per_wave": args.tau_per_wave, "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4), "traffic": profiled_traffic(w.name, head)},
     }

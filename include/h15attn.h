@@ -72,7 +72,8 @@ enum attn_expmode { ATTN_EXP_EXACT = 0, ATTN_EXP_H15 = 1, ATTN_EXP_SQ4 = 2, ATTN
 enum attn_status {
     ATTN_OK = 0,
     ATTN_EINVAL = -1,      /* null pointer, non-positive size, Hq % Hkv != 0,
-                              scale or descale not positive and finite */
+                              scale or descale not positive and finite,
+                              rescale_threshold outside [0, 64] */
     ATTN_EUNSUPPORTED = -2, /* d not in {64, 128}, unknown dtype or exp_mode,
                               pointer not 16-byte aligned, B*Hq*S > 2^30, or
                               one head's K/V rows (S * d * element bytes)
@@ -82,10 +83,26 @@ enum attn_status {
 
 /* Optional per-call settings.  FP8 requires the three per-tensor descales
  * (the factors that turn stored e4m3 values back into real values); BF16
- * ignores them.  stream is a hipStream_t (NULL: default stream). */
+ * ignores them.  stream is a hipStream_t (NULL: default stream).
+ *
+ * rescale_threshold (tau, base-two units, default 0) is the conditional
+ * rescale of App. B.2 ("Conditional rescaling moves the anchor"): at each key
+ * tile the running maximum m moves to max(m, mt) only when it grows by more
+ * than tau, g = fp32(fp32(mt - m) * c1) > tau (the first tile always sets
+ * it); otherwise the anchor stays and the weights of the tile are taken
+ * relative to it (they may exceed 2^off, up to about 2^(tau + off)).  With
+ * rescale_per_wave = 0 each row decides for itself (the paper's semantic
+ * simulation); with 1 the decision is shared by each aligned group of 32
+ * query rows (rows 32w .. 32w + 31 of a head), moving every row's anchor when
+ * any real row of the group grows by more than tau (FlashAttention-4's
+ * per-warp decision).  tau must be finite, 0 <= tau <= 64 (else
+ * ATTN_EINVAL); FP8 requires tau = 0 (P must stay within e4m3's range; else
+ * ATTN_EUNSUPPORTED).  A zero-initialised struct gives tau = 0. */
 typedef struct attn_opts {
     float q_descale, k_descale, v_descale;
     void* stream;
+    float rescale_threshold;
+    int rescale_per_wave;
 } attn_opts;
 
 /* Attention forward on the default stream with unit descales. */

@@ -26,7 +26,8 @@ EXPORTS = ("attn_fwd", "attn_fwd_ex", "attn_fwd_probe", "attn_strerror", "attn_t
 
 class attn_opts(ctypes.Structure):
     _fields_ = [("q_descale", ctypes.c_float), ("k_descale", ctypes.c_float),
-                ("v_descale", ctypes.c_float), ("stream", ctypes.c_void_p)]
+                ("v_descale", ctypes.c_float), ("stream", ctypes.c_void_p),
+                ("rescale_threshold", ctypes.c_float), ("rescale_per_wave", ctypes.c_int)]
 
 
 class AttnError(RuntimeError):
@@ -103,19 +104,21 @@ def _outputs(q, out, lse, want_lse):
     return out, lse
 
 
-def _opts(descale, stream):
+def _opts(descale, stream, tau=0.0, tau_per_wave=False):
     import torch
     qd, kd, vd = descale if descale is not None else (1.0, 1.0, 1.0)
     st = stream if stream is not None else torch.cuda.current_stream()
-    return attn_opts(float(qd), float(kd), float(vd), ctypes.c_void_p(st.cuda_stream))
+    return attn_opts(float(qd), float(kd), float(vd), ctypes.c_void_p(st.cuda_stream), float(tau),
+                     int(bool(tau_per_wave)))
 
 
 def attn_fwd_ex(q, k, v, *, causal: bool, scale: float, exp_mode: int, descale=None, stream=None,
-                out=None, lse=None, want_lse: bool = True):
-    """O (and LSE) of attention; see include/h15attn.h for the definition."""
+                out=None, lse=None, want_lse: bool = True, tau: float = 0.0, tau_per_wave: bool = False):
+    """O (and LSE) of attention; see include/h15attn.h for the definition.
+    tau / tau_per_wave: the conditional-rescale threshold and its granularity."""
     B, Hq, Hkv, S, d, dt = _check(q, k, v)
     out, lse = _outputs(q, out, lse, want_lse)
-    opts = _opts(descale, stream)
+    opts = _opts(descale, stream, tau, tau_per_wave)
     rc = lib().attn_fwd_ex(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
                            lse.data_ptr() if lse is not None else None, B, Hq, Hkv, S, d,
                            int(bool(causal)), float(scale), dt, int(exp_mode), ctypes.byref(opts))
@@ -138,7 +141,8 @@ def attn_fwd(q, k, v, *, causal: bool, scale: float, exp_mode: int, out=None, ls
 
 
 def attn_fwd_probe(q, k, v, *, causal: bool, scale: float, exp_mode: int, b: int, h: int,
-                   row0: int, nrows: int, descale=None, stream=None):
+                   row0: int, nrows: int, descale=None, stream=None, tau: float = 0.0,
+                   tau_per_wave: bool = False):
     """Returns (O, LSE, s, w, p_bits) with s/w/p_bits of shape [nrows, S]."""
     import torch
     B, Hq, Hkv, S, d, dt = _check(q, k, v)
@@ -146,7 +150,7 @@ def attn_fwd_probe(q, k, v, *, causal: bool, scale: float, exp_mode: int, b: int
     s = torch.empty((nrows, S), dtype=torch.float32, device=q.device)
     w = torch.empty((nrows, S), dtype=torch.float32, device=q.device)
     pb = torch.empty((nrows, S), dtype=torch.int32, device=q.device)
-    opts = _opts(descale, stream)
+    opts = _opts(descale, stream, tau, tau_per_wave)
     rc = lib().attn_fwd_probe(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(),
                               B, Hq, Hkv, S, d, int(bool(causal)), float(scale), dt, int(exp_mode),
                               ctypes.byref(opts), int(b), int(h), int(row0), int(nrows),

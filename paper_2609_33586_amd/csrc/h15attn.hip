@@ -81,6 +81,8 @@ struct Params {
   float* lse;
   int B, Hq, Hkv, S, G;
   float c1, ck, vd;  // base-two logit scale; 2^k c1 for the weight; V descale
+  float tau;          // conditional-rescale threshold (0: the anchor is the running max)
+  int tau_wave;       // 1: the anchor decision is shared by the wave's 32 rows
   int nqb;    // query blocks per head
   int remap;  // XCD-grouped workgroup order is valid for this shape
   // probe target (PROBE instantiations only)
@@ -529,7 +531,16 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
     const float mt = tile_max(sacc);
     float ma, mb;
     with_partner(mt, ma, mb);
-    const float m_new = max3(m_run, ma, mb);
+    float m_new = max3(m_run, ma, mb);
+    if (DT == DT_BF16 && p.tau > 0.0f) {
+      // conditional rescale (App. B.2; FP8 requires tau = 0): the anchor
+      // moves only when the row's maximum grows by more than tau octaves
+      // (FP32 test); per wave, when any real row of the wave does
+      const float grow_by = (__builtin_fmaxf(ma, mb) - m_run) * p.c1;
+      bool move = m_run == -INFINITY || grow_by > p.tau;
+      if (p.tau_wave) move = __builtin_amdgcn_ballot_w64(move && qrow < S) != 0;
+      if (!move) m_new = m_run;
+    }
     const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * p.c1);
     m_run = m_new;
 
@@ -755,8 +766,11 @@ int fill_params(Params& p, const void* q, const void* k, const void* v, void* o,
   if (mis & 15u) return ATTN_EUNSUPPORTED;
   if (lse && ((uintptr_t)lse & 3u)) return ATTN_EUNSUPPORTED;
   float qd = 1.0f, kd = 1.0f, vd = 1.0f;
+  const float tau = opts ? opts->rescale_threshold : 0.0f;
+  if (!(tau >= 0.0f && tau <= 64.0f)) return ATTN_EINVAL;
   if (dtype == ATTN_FP8_E4M3) {
     if (!opts) return ATTN_EINVAL;
+    if (tau != 0.0f) return ATTN_EUNSUPPORTED;
     qd = opts->q_descale;
     kd = opts->k_descale;
     vd = opts->v_descale;
@@ -783,6 +797,8 @@ int fill_params(Params& p, const void* q, const void* k, const void* v, void* o,
   p.c1 = (float)((double)scale * (double)qd * (double)kd * 1.4426950408889634);
   p.ck = ldexpf(p.c1, exp_order(exp_mode));
   p.vd = vd;
+  p.tau = tau;
+  p.tau_wave = (opts && opts->rescale_per_wave) ? 1 : 0;
   p.nqb = (S + row_block(dtype) - 1) / row_block(dtype);
   p.remap = ((B * Hkv) % 8 == 0) ? 1 : 0;
   return ATTN_OK;

@@ -71,6 +71,16 @@ def test_invalid_arguments(L):
         assert call(L, dtype=1, opts=pkg.attn_opts(*bad, None)) == E_INV
 
 
+def test_rescale_threshold_validation(L):
+    E_INV, E_UNS = pkg.ATTN_EINVAL, pkg.ATTN_EUNSUPPORTED
+    for tau in (-1.0, -1e-30, 64.5, math.inf, math.nan):
+        assert call(L, opts=pkg.attn_opts(1.0, 1.0, 1.0, None, tau, 0)) == E_INV
+        assert call(L, dtype=1, opts=pkg.attn_opts(1.0, 1.0, 1.0, None, tau, 1)) == E_INV
+    # FP8 P must stay within e4m3's range: only tau = 0
+    for tau in (0.5, 8.0):
+        assert call(L, dtype=1, opts=pkg.attn_opts(1.0, 1.0, 1.0, None, tau, 0)) == E_UNS
+
+
 def test_probe_invalid_rows(L):
     opts = pkg.attn_opts(1.0, 1.0, 1.0, None)
     args = [FAKE, FAKE, FAKE, FAKE, None, 1, 2, 1, 64, 128, 0, 0.1, 0, 1, ctypes.byref(opts)]
