@@ -63,6 +63,8 @@ def lib() -> ctypes.CDLL:
     L.oracle_sq_count_mismatch.restype = c_i64
     L.oracle_sq_row_from_logits.argtypes = [c_p, c_i, c_i, c_i, c_f, c_i, c_i, c_d, c_i, c_i, c_p, c_p, c_p]
     L.oracle_sq_row_from_logits.restype = c_i
+    L.oracle_pot_row_from_logits.argtypes = [c_p, c_i, c_i, c_i, c_f, c_p, c_p, c_p]
+    L.oracle_pot_row_from_logits.restype = c_i
     L.oracle_c1.argtypes = [c_d, c_d, c_d]
     L.oracle_c1.restype = c_f
     L.oracle_h15_row_from_logits.argtypes = [c_p, c_i, c_i, c_i, c_f, c_i, c_i, c_d, c_i, c_p, c_p, c_p]
@@ -204,6 +206,20 @@ def sq_row_from_logits_moves(s: np.ndarray, i: int, causal: bool, c1_: float, dt
                                                int(Bc), _ptr(move), int(k), _ptr(w), _ptr(p), ctypes.byref(lse))
     if rc != 0:
         raise ValueError("oracle_sq_row_from_logits_moves: invalid arguments")
+    return w, p, lse.value
+
+
+def pot_row_from_logits(s: np.ndarray, i: int, causal: bool, c1_: float):
+    """Rowmax-PoT (Eq. (rowmax-pot), K_max = 20) W, P (bf16 bits) and LSE of row i from fp32 logits."""
+    s = np.ascontiguousarray(s, dtype=np.float32)
+    S = s.shape[0]
+    w = np.zeros(S, np.float32)
+    p = np.zeros(S, np.uint32)
+    lse = ctypes.c_double(0.0)
+    rc = lib().oracle_pot_row_from_logits(_ptr(s), S, int(i), int(bool(causal)), float(c1_), _ptr(w), _ptr(p),
+                                          ctypes.byref(lse))
+    if rc != 0:
+        raise ValueError("oracle_pot_row_from_logits: invalid arguments")
     return w, p, lse.value
 
 

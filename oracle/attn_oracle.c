@@ -356,6 +356,40 @@ int oracle_sq_row_from_logits_moves(const float* s, int S, int i, int causal, fl
     return 0;
 }
 
+/* Rowmax-PoT (App. A.6 Eq. (rowmax-pot)) of one query row from its fp32
+ * logits, in the arithmetic a kernel can reproduce: the anchor m is the
+ * row's maximum raw logit over its valid keys, the base-two gap is
+ * x_j = fp32(fp32(m - s_j) * c1) (the paper's Delta_j / ln 2 with
+ * c1 = fp32(scale qd kd log2 e)), d_j = min(K_max, floor(x_j + 1/2)) with
+ * K_max = 20 (x_j + 1/2 is exact in fp32 below 2^22), w_j = 2^-d_j, and
+ * masked keys carry w = P = 0.  P is w in the operand type (BF16 only: every
+ * level 2^0 .. 2^-20 is exact there).  l sums w; LSE = ln2 (m c1 + log2 l). */
+int oracle_pot_row_from_logits(const float* s, int S, int i, int causal, float c1, float* w_out,
+                               uint32_t* p_out, double* lse_out)
+{
+    if (S <= 0 || i < 0 || i >= S) return -1;
+    const int jend = causal ? i + 1 : S;
+    float m = -INFINITY;
+    for (int j = 0; j < jend; j++) m = fmaxf(m, s[j]);
+    double l = 0.0;
+    for (int j = 0; j < S; j++) {
+        float w = 0.0f;
+        if (j < jend) {
+            volatile float gap = m - s[j];
+            volatile float x = gap * c1;
+            volatile float t = x + 0.5f;
+            float d = floorf(t);
+            if (d > 20.0f) d = 20.0f;
+            w = ldexpf(1.0f, -(int)d);
+        }
+        l += (double)w;
+        if (w_out) w_out[j] = w;
+        if (p_out) p_out[j] = bf16_rne(w);
+    }
+    if (lse_out) *lse_out = M_LN2 * ((double)m * (double)c1 + log2(l));
+    return 0;
+}
+
 int oracle_h15_row_from_logits(const float* s, int S, int i, int causal, float c1, int dtype,
                                int Bc, double tau, int exact_exp, float* w_out, uint32_t* p_out,
                                double* lse_out)

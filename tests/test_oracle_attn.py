@@ -313,3 +313,35 @@ def test_exact_tile_close_to_exact():
     b, _ = oracle.attn(inp.q, inp.k, inp.v, dtype=BF16, causal=True, scale=0.18, mode=oracle.EXACT_TILE, Bc=32)
     vmax = np.max(np.abs(synth.bf16_decode(inp.v)))
     assert np.max(np.abs(a - b)) < 2.0 ** -8 * vmax
+
+
+def test_rowmax_pot_row_from_logits_closed_forms():
+    # the kernel-arithmetic form of Eq. (rowmax-pot): c1 = 1 makes x_j = m - s_j
+    s = np.array([0.0, -1.0, -2.5, -25.0, -3.25, -0.5, -1.5, -19.5, -19.49], np.float32)
+    w, p, lse = oracle.pot_row_from_logits(s, 8, False, 1.0)
+    d = np.array([0, 1, 3, 20, 3, 1, 2, 20, 19])  # half rounds up; the tail clamps at 20
+    assert np.array_equal(w, (2.0 ** -d).astype(np.float32))
+    assert np.array_equal(p, np.array([int(np.array([x], np.float32).view(np.uint32)[0]) >> 16 for x in w]))
+    assert abs(lse - math.log(2) * math.log2(np.sum(2.0 ** -d))) < 1e-14
+    # causal: keys after the row carry nothing, and the anchor is the row's own max
+    w, p, _ = oracle.pot_row_from_logits(np.array([-1.0, -3.0, 5.0], np.float32), 1, True, 1.0)
+    assert list(w) == [1.0, 0.25, 0.0] and p[2] == 0
+    # a shift of every logit by an exactly representable constant changes nothing
+    w2, _, _ = oracle.pot_row_from_logits(s + np.float32(64.0), 8, False, 1.0)
+    assert np.array_equal(w2, oracle.pot_row_from_logits(s, 8, False, 1.0)[0])
+
+
+def test_rowmax_pot_row_form_matches_fp64_operator():
+    # integer logits and c1 = 1: every gap is exact in both arithmetics, so
+    # the row form's weights give the fp64 operator's O and LSE
+    rng = np.random.default_rng(41)
+    inp = integer_inputs(1, 2, 1, 40, 4, rng, lo=-3, hi=3)
+    o, lse = oracle.attn(inp.q, inp.k, inp.v, dtype=BF16, causal=True, scale=SCALE_C1_ONE, mode=oracle.ROWMAX_POT)
+    _, _, vdq = dequant(inp)
+    for h in range(2):
+        for i in (0, 9, 39):
+            s = oracle.logits_row(inp.q, inp.k, BF16, 0, h, i)
+            w, _, lse_row = oracle.pot_row_from_logits(s, i, True, 1.0)
+            w = w.astype(np.float64)
+            assert np.max(np.abs(o[0, h, i] - (w @ vdq[0, 0]) / w.sum())) < 1e-12
+            assert abs(lse[0, h, i] - lse_row) < 1e-12
