@@ -38,8 +38,9 @@ def parse():
     ap.add_argument("--rounds", type=int, default=3)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU baseline sample time")
-    ap.add_argument("--modes", default="h15,exact,sq4,sq8",
-                    help="weights to time: h15 (the method), exact (control), sq4/sq8 (S(Q_1/4), S(Q_1/8))")
+    ap.add_argument("--modes", default=None,
+                    help="weights to time: h15 (the method), exact (control), sq4/sq8 (S(Q_1/4), S(Q_1/8)), "
+                         "pot (Rowmax-PoT, BF16 only); default all that the operand type supports")
     ap.add_argument("--tau", type=float, default=0.0,
                     help="conditional-rescale threshold in octaves (BF16 workloads only; 0 = running max)")
     ap.add_argument("--tau-per-wave", action="store_true", help="share the rescale decision per 32-row wave")
@@ -132,7 +133,9 @@ def main():
     lse = torch.empty((w.B, w.Hq, w.S), dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
     modes = {"h15": pkg.ATTN_EXP_H15, "exact": pkg.ATTN_EXP_EXACT, "sq4": pkg.ATTN_EXP_SQ4, "sq8": pkg.ATTN_EXP_SQ8}
-    want = [m for m in args.modes.split(",") if m in modes]
+    if w.dtype == synth.BF16:
+        modes["pot"] = pkg.ATTN_EXP_ROWMAX_POT
+    want = [m for m in (args.modes or ",".join(modes)).split(",") if m in modes]
 
     if args.tau != 0.0 and w.dtype != synth.BF16:
         print("bench.py: --tau applies to BF16 workloads only (FP8 keeps the running max)", file=sys.stderr)
@@ -204,12 +207,12 @@ def main():
             "h15_vs_exact_speedup_pct": round(100.0 * (med["exact"] / med["h15"] - 1.0), 2),
             "windows_ms_per_call": {m: [round(t / n, 5) for t, n in windows[m]] for m in want},
         }
-    variants = [m for m in ("sq4", "sq8") if m in want]
+    variants = [m for m in ("sq4", "sq8", "pot") if m in want]
     if variants and "h15" in want:
-        # App. B.2's finer input rounding S(Q_{2^-k}), k = 2, 3: same kernel,
-        # timed in the same alternating rounds
+        # App. B.2's finer input rounding S(Q_{2^-k}), k = 2, 3, and Rowmax-PoT
+        # (App. A.6): same kernel, timed in the same alternating rounds
         med = {m: float(np.median([t / n for t, n in windows[m]])) for m in want}
-        line["input_rounding_variants"] = {
+        line["weight_variants"] = {
             m: {"ms_per_call": round(res_ms[m], 5), "tflops": round(tflops[m], 2),
                 "vs_h15_pct": round(100.0 * (med["h15"] / med[m] - 1.0), 2)} for m in variants}
     if not args.no_cpu:

@@ -27,6 +27,12 @@
  *                   w = bits^-1((bits(t) << (23 - k)) + bits(1.0f)).
  *                   Every weight has at most k mantissa bits, so P = w is
  *                   exact in bf16, and in e4m3 from 2^-6 up.
+ *   ATTN_EXP_ROWMAX_POT: Rowmax-PoT (App. A.6 Eq. (rowmax-pot)), anchored at
+ *                   the whole-row maximum m of the raw logits (a first pass
+ *                   over the key tiles computes it, so the running maximum
+ *                   never moves): x = fp32(fp32(m - s_ij) * c1),
+ *                   d = min(20, floor(x + 1/2)), w = 2^-d.  BF16 only (the 21
+ *                   levels are exact in bf16; e4m3 spans under 18 octaves).
  * where s_ij = sum_c q_ic k_jc is the raw logit of the stored operands (bf16
  * values, or e4m3 values without their descales) accumulated in fp32,
  * c1 = fp32(scale * q_descale * k_descale * log2(e)) (products in double,
@@ -68,7 +74,13 @@ extern "C" {
 #endif
 
 enum attn_dtype { ATTN_BF16 = 0, ATTN_FP8_E4M3 = 1 };
-enum attn_expmode { ATTN_EXP_EXACT = 0, ATTN_EXP_H15 = 1, ATTN_EXP_SQ4 = 2, ATTN_EXP_SQ8 = 3 };
+enum attn_expmode {
+    ATTN_EXP_EXACT = 0,
+    ATTN_EXP_H15 = 1,
+    ATTN_EXP_SQ4 = 2,
+    ATTN_EXP_SQ8 = 3,
+    ATTN_EXP_ROWMAX_POT = 4 /* BF16 only, rescale_threshold 0 (else ATTN_EUNSUPPORTED) */
+};
 enum attn_status {
     ATTN_OK = 0,
     ATTN_EINVAL = -1,      /* null pointer, non-positive size, Hq % Hkv != 0,

@@ -17,7 +17,7 @@ _PKG = Path(__file__).resolve().parent
 LIB_PATH = _PKG / "libh15attn.so"
 
 ATTN_BF16, ATTN_FP8_E4M3 = 0, 1
-ATTN_EXP_EXACT, ATTN_EXP_H15, ATTN_EXP_SQ4, ATTN_EXP_SQ8 = 0, 1, 2, 3
+ATTN_EXP_EXACT, ATTN_EXP_H15, ATTN_EXP_SQ4, ATTN_EXP_SQ8, ATTN_EXP_ROWMAX_POT = 0, 1, 2, 3, 4
 ATTN_OK, ATTN_EINVAL, ATTN_EUNSUPPORTED, ATTN_ELAUNCH = 0, -1, -2, -3
 
 # every symbol the header declares

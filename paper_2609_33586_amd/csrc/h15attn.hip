@@ -69,9 +69,12 @@ constexpr uint32_t CLAMP_BIAS = 0x00800000u;
 // family S(Q_{2^-k}) (App. B.2; k = 1 is Rowmax-H15, App. B.1) takes mode
 // 2k - 1 with the clamp in floating point and 2k with the clamp on the
 // integer form (exact only when y + 0x1.8p23 >= 0 for every score).
-enum { MODE_EXACT = 0, MODE_H15 = 1, MODE_H15_FASTCLAMP = 2 };
+// Mode 7 is Rowmax-PoT (App. A.6 Eq. (rowmax-pot)), anchored at the whole-row
+// maximum, BF16 only.
+enum { MODE_EXACT = 0, MODE_H15 = 1, MODE_H15_FASTCLAMP = 2, MODE_ROWMAX_POT = 7 };
 constexpr int mode_order(int mode) { return (mode + 1) / 2; }
-constexpr bool mode_intclamp(int mode) { return mode != MODE_EXACT && mode % 2 == 0; }
+constexpr bool mode_intclamp(int mode) { return mode != MODE_EXACT && mode != MODE_ROWMAX_POT && mode % 2 == 0; }
+constexpr int POT_KMAX = 20;  // tail clamp of Rowmax-PoT
 
 struct Params {
   const uint8_t* q;
@@ -165,6 +168,15 @@ __device__ __forceinline__ float sq_weight(float s, float ck, float nbk) {
     const float t = __builtin_fmaxf(y, -126.0f * (float)(1 << K)) + H15_MAGIC;
     return __uint_as_float((__float_as_uint(t) << (23 - K)) + ONE_BITS);
   }
+}
+
+// Rowmax-PoT weight of one score (App. A.6 Eq. (rowmax-pot)) against the
+// whole-row maximum m: base-two gap x = fp32(fp32(m - s) c1), d = min(K_max,
+// floor(x + 1/2)) (exact: x + 1/2 is representable below 2^22), w = 2^-d.
+__device__ __forceinline__ float pot_weight(float s, float m, float c1) {
+  const float x = (m - s) * c1;
+  const float d = __builtin_fminf(__builtin_floorf(x + 0.5f), (float)POT_KMAX);
+  return __builtin_amdgcn_ldexpf(1.0f, -(int)d);
 }
 
 // x, or y where key offset C lies beyond this lane's last valid offset lim.
@@ -501,17 +513,25 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
     }
   };
 
+  // ---- masked keys (causal diagonal, ragged tail) of tile t get score -inf;
+  // returns whether the tile needed masking
+  auto mask_scores = [&](int t) {
+    const int kt0 = t * BC;
+    const bool need_mask = (CAUSAL && kt0 + BC - 1 > qw0) || (kt0 + BC > S);
+    if (need_mask) {
+      const int lim = (CAUSAL ? min(qrow, S - 1) : S - 1) - kt0 - 4 * g;
+      mask_beyond(sacc, lim, -INFINITY);
+    }
+    return need_mask;
+  };
+
   // ---- the scores of tile t become weights, the running state moves, and P
   // is left in pb/pf for the PV product
   auto softmax_tile = [&](int t) {
     const int kt0 = t * BC;
 
     // masking: causal diagonal and the ragged tail only
-    const bool need_mask = (CAUSAL && kt0 + BC - 1 > qw0) || (kt0 + BC > S);
-    if (need_mask) {
-      const int lim = (CAUSAL ? min(qrow, S - 1) : S - 1) - kt0 - 4 * g;
-      mask_beyond(sacc, lim, -INFINITY);
-    }
+    const bool need_mask = mask_scores(t);
 
     const bool probe_row = PROBE && b == p.pb && h == p.ph && qrow >= p.prow0 && qrow < p.prow0 + p.pnrows;
     if constexpr (PROBE) {
@@ -527,30 +547,41 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
       }
     }
 
-    // running maximum (threshold 0: moves to the maximum so far)
-    const float mt = tile_max(sacc);
-    float ma, mb;
-    with_partner(mt, ma, mb);
-    float m_new = max3(m_run, ma, mb);
-    if (DT == DT_BF16 && p.tau > 0.0f) {
-      // conditional rescale (App. B.2; FP8 requires tau = 0): the anchor
-      // moves only when the row's maximum grows by more than tau octaves
-      // (FP32 test); per wave, when any real row of the wave does
-      const float grow_by = (__builtin_fmaxf(ma, mb) - m_run) * p.c1;
-      bool move = m_run == -INFINITY || grow_by > p.tau;
-      if (p.tau_wave) move = __builtin_amdgcn_ballot_w64(move && qrow < S) != 0;
-      if (!move) m_new = m_run;
+    // running maximum (threshold 0: moves to the maximum so far); Rowmax-PoT
+    // keeps the whole-row maximum of its first pass
+    float m_new = m_run;
+    if constexpr (MODE != MODE_ROWMAX_POT) {
+      const float mt = tile_max(sacc);
+      float ma, mb;
+      with_partner(mt, ma, mb);
+      m_new = max3(m_run, ma, mb);
+      if (DT == DT_BF16 && p.tau > 0.0f) {
+        // conditional rescale (App. B.2; FP8 requires tau = 0): the anchor
+        // moves only when the row's maximum grows by more than tau octaves
+        // (FP32 test); per wave, when any real row of the wave does
+        const float grow_by = (__builtin_fmaxf(ma, mb) - m_run) * p.c1;
+        bool move = m_run == -INFINITY || grow_by > p.tau;
+        if (p.tau_wave) move = __builtin_amdgcn_ballot_w64(move && qrow < S) != 0;
+        if (!move) m_new = m_run;
+      }
     }
     const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * p.c1);
     m_run = m_new;
 
     // weights, in place over the scores
     if constexpr (MODE != MODE_EXACT) {
-      const float nbk = __builtin_fmaf(-m_new, p.ck, (float)(1 << mode_order(MODE)) * off);
+      if constexpr (MODE == MODE_ROWMAX_POT) {
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
+        for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int j = 0; j < 16; ++j) sacc[kb][j] = sq_weight<MODE>(sacc[kb][j], p.ck, nbk);
+          for (int j = 0; j < 16; ++j) sacc[kb][j] = pot_weight(sacc[kb][j], m_new, p.c1);
+      } else {
+        const float nbk = __builtin_fmaf(-m_new, p.ck, (float)(1 << mode_order(MODE)) * off);
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int j = 0; j < 16; ++j) sacc[kb][j] = sq_weight<MODE>(sacc[kb][j], p.ck, nbk);
+      }
       if (need_mask) {
         // masked keys carry weight 0 (the clamp alone would give 2^-126)
         const int lim = (CAUSAL ? min(qrow, S - 1) : S - 1) - kt0 - 4 * g;
@@ -618,6 +649,29 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
 
   // last tile holding a valid key for some row of this wave (-1: none)
   const int last_act = !wave_live ? -1 : (CAUSAL ? min(ntiles - 1, (qw0 + WROWS - 1) / BC) : ntiles - 1);
+  if constexpr (MODE == MODE_ROWMAX_POT) {
+    // ---- Rowmax-PoT anchors every weight at the whole-row maximum: a first
+    // pass over the key tiles computes it (QK^T and the masked row max only)
+    stage_k(0, ALL_WAVES, 0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    for (int t = 0; t < ntiles; ++t) {
+      if (t + 1 < ntiles) stage_k(t + 1, ALL_WAVES, 0);
+      if (t <= last_act) {
+        __builtin_amdgcn_s_setprio(1);
+        qk(kbuf(t));
+        __builtin_amdgcn_s_setprio(0);
+        mask_scores(t);
+        const float mt = tile_max(sacc);
+        float ma, mb;
+        with_partner(mt, ma, mb);
+        m_run = max3(m_run, ma, mb);
+      }
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+    }
+  }
+
   // ---- one tile per step: copy in the next tile, then QK^T, weights, PV
   stage_k(0, ALL_WAVES, 0);
   stage_v(0, ALL_WAVES, 0);
@@ -695,6 +749,9 @@ hipError_t launch_mode(const Params& p, int mode, hipStream_t st) {
     case 5: return launch_one<DT, D, CAUSAL, 5, PROBE>(p, st);
     default: break;
   }
+  if constexpr (DT == DT_BF16) {
+    if (mode == MODE_ROWMAX_POT) return launch_one<DT, D, CAUSAL, MODE_ROWMAX_POT, PROBE>(p, st);
+  }
   // the integer-clamp forms are only ever chosen for FP8
   if constexpr (DT == DT_FP8) {
     switch (mode) {
@@ -738,6 +795,7 @@ int exp_order(int exp_mode) {
 // that is below 2^22 the exponent y + 0x1.8p23 can never go negative and the
 // integer form of the clamp gives exactly the canonical bits.
 int kernel_mode(int dtype, int exp_mode, int d, float ck) {
+  if (exp_mode == ATTN_EXP_ROWMAX_POT) return MODE_ROWMAX_POT;
   const int k = exp_order(exp_mode);
   if (k == 0) return MODE_EXACT;
   if (dtype == ATTN_FP8_E4M3) {
@@ -760,7 +818,12 @@ int fill_params(Params& p, const void* q, const void* k, const void* v, void* o,
   if (Hq % Hkv != 0) return ATTN_EINVAL;
   if (!finite_pos(scale)) return ATTN_EINVAL;
   if (dtype != ATTN_BF16 && dtype != ATTN_FP8_E4M3) return ATTN_EUNSUPPORTED;
-  if (exp_mode != ATTN_EXP_EXACT && exp_order(exp_mode) == 0) return ATTN_EUNSUPPORTED;
+  if (exp_mode != ATTN_EXP_EXACT && exp_mode != ATTN_EXP_ROWMAX_POT && exp_order(exp_mode) == 0)
+    return ATTN_EUNSUPPORTED;
+  // Rowmax-PoT: 21 levels 2^0 .. 2^-20 need bf16's range for P (e4m3 spans
+  // under 18 octaves); its anchor is the whole-row maximum, so no threshold
+  if (exp_mode == ATTN_EXP_ROWMAX_POT && (dtype != ATTN_BF16 || (opts && opts->rescale_threshold != 0.0f)))
+    return ATTN_EUNSUPPORTED;
   if (d != 64 && d != 128) return ATTN_EUNSUPPORTED;
   const uintptr_t mis = (uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)o;
   if (mis & 15u) return ATTN_EUNSUPPORTED;

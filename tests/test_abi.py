@@ -81,6 +81,14 @@ def test_rescale_threshold_validation(L):
         assert call(L, dtype=1, opts=pkg.attn_opts(1.0, 1.0, 1.0, None, tau, 0)) == E_UNS
 
 
+def test_rowmax_pot_is_bf16_only(L):
+    E_UNS = pkg.ATTN_EUNSUPPORTED
+    pot = pkg.ATTN_EXP_ROWMAX_POT
+    assert call(L, dtype=1, mode=pot, opts=pkg.attn_opts(1.0, 1.0, 1.0, None, 0.0, 0)) == E_UNS
+    assert call(L, dtype=0, mode=pot, opts=pkg.attn_opts(1.0, 1.0, 1.0, None, 8.0, 0)) == E_UNS
+    assert call(L, mode=5) == E_UNS
+
+
 def test_probe_invalid_rows(L):
     opts = pkg.attn_opts(1.0, 1.0, 1.0, None)
     args = [FAKE, FAKE, FAKE, FAKE, None, 1, 2, 1, 64, 128, 0, 0.1, 0, 1, ctypes.byref(opts)]

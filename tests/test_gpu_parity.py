@@ -10,7 +10,9 @@ by the fp32 accumulation order of the logit, moves LSE by a fraction of that
 weight), and against the oracle fed the GPU's own logits to 1e-5.  The H15
 weights and stored P are compared bit for bit when the oracle is fed the
 GPU's own fp32 logits.  The finer input-rounding weights S(Q_{2^-k}) for
-k = 2, 3 (exp modes SQ4, SQ8) are held to the same bars as H15."""
+k = 2, 3 (exp modes SQ4, SQ8) are held to the same bars as H15, and so is
+Rowmax-PoT (BF16) against the fp64 operator of Eq. (rowmax-pot), with its W
+and P bit-exact against the row form of the oracle fed the GPU's logits."""
 import math
 import sys
 
@@ -28,7 +30,9 @@ BF16, FP8 = synth.BF16, synth.FP8_E4M3
 EXACT, H15, SQ4, SQ8 = pkg.ATTN_EXP_EXACT, pkg.ATTN_EXP_H15, pkg.ATTN_EXP_SQ4, pkg.ATTN_EXP_SQ8
 APPROX = (H15, SQ4, SQ8)
 ALL_MODES = (EXACT,) + APPROX
-ORACLE_MODE = {EXACT: oracle.EXACT, H15: oracle.H15_TILE, SQ4: oracle.SQ4_TILE, SQ8: oracle.SQ8_TILE}
+POT = pkg.ATTN_EXP_ROWMAX_POT  # BF16 only
+ORACLE_MODE = {EXACT: oracle.EXACT, H15: oracle.H15_TILE, SQ4: oracle.SQ4_TILE, SQ8: oracle.SQ8_TILE,
+               POT: oracle.ROWMAX_POT}
 ORDER = {H15: 1, SQ4: 2, SQ8: 3}  # input-rounding exponent k
 TOL = {BF16: 2e-2, FP8: 6e-2}
 LSE_TOL = 1e-3
@@ -78,7 +82,7 @@ def assert_close(inp, o, lse, o_ref, lse_ref, what, mode=EXACT):
         f"rows |dLSE|>1e-4: {np.mean(dl > 1e-4):.4f}")
     assert np.all(np.isfinite(o)) and np.all(np.isfinite(lse))
     assert err <= bound, what
-    if mode in APPROX:
+    if mode in APPROX or mode == POT:
         # Against the oracle's own logits, a few weights sit on the other side
         # of an RNE boundary (fp32 accumulation order of the logits), which
         # moves LSE by a fraction of one weight; the exact LSE check is the
@@ -307,3 +311,63 @@ def test_side_stream_and_lse_optional():
     st.synchronize()
     torch.cuda.synchronize()
     assert torch.equal(o_ref.view(torch.int16), o2.view(torch.int16))
+
+
+# ---- Rowmax-PoT (App. A.6 Eq. (rowmax-pot)), BF16 --------------------------
+
+@pytest.mark.parametrize("d,causal,S", [(64, False, 256), (64, True, 300), (128, False, 300), (128, True, 520)])
+def test_rowmax_pot_small_full_parity(d, causal, S):
+    inp = synth.make_inputs(1, 4, 2, S, d, BF16, sharp=True, seed=800 + S + d)
+    sc = scale_of(d)
+    say(f"rowmax-pot d={d} causal={causal} S={S}")
+    o, lse = gpu_run(inp, causal, sc, POT)
+    o_ref, lse_ref = oracle_run(inp, causal, sc, POT)
+    assert_close(inp, o, lse, o_ref.reshape(o.shape), lse_ref.reshape(lse.shape), "rowmax-pot", POT)
+
+
+def check_pot_probe(inp, S, causal, sc, rowsets):
+    q, k, v = dev_tensors(inp)
+    c1 = oracle.c1(sc)
+    for (b, h, r0, n) in rowsets:
+        say(f"rowmax-pot probe causal={causal} head {h} rows {r0}+{n}")
+        o_p, lse_p, s, w, pbits = pkg.attn_fwd_probe(q, k, v, causal=causal, scale=sc, exp_mode=POT, b=b, h=h,
+                                                     row0=r0, nrows=n)
+        o_m, lse_m = pkg.attn_fwd_ex(q, k, v, causal=causal, scale=sc, exp_mode=POT)
+        torch.cuda.synchronize()
+        assert torch.equal(o_p.view(torch.int16), o_m.view(torch.int16)) and torch.equal(lse_p, lse_m)
+        s, w, pbits, lse_p = s.cpu().numpy(), w.cpu().numpy(), pbits.cpu().numpy().astype(np.uint32), lse_p.cpu().numpy()
+        for r in range(n):
+            i = r0 + r
+            w_ref, p_ref, lse_ref = oracle.pot_row_from_logits(np.where(np.isneginf(s[r]), np.float32(0), s[r]), i,
+                                                                causal, c1)
+            assert np.array_equal(w[r].view(np.uint32), w_ref.view(np.uint32)), f"row {i}"
+            assert np.array_equal(pbits[r], p_ref), f"row {i}"
+            assert abs(lse_p[b, h, i] - lse_ref) <= 1e-5, f"row {i}"
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_rowmax_pot_probe_bit_exact(causal):
+    S = 520
+    inp = synth.make_inputs(1, 4, 1, S, 128, BF16, sharp=True, seed=801)
+    check_pot_probe(inp, S, causal, scale_of(128), ((0, 0, 0, 40), (0, 3, 250, 40), (0, 2, S - 37, 37)))
+
+
+POT_FULL = [synth.WORKLOADS[n] for n in ("causal_bf16_b4_h32kv8_s2048_d128_sharp",
+                                         "causal_bf16_b1_h64kv8_s16384_d128_sharp")]
+
+
+@pytest.mark.parametrize("w", POT_FULL, ids=[w.name for w in POT_FULL])
+def test_rowmax_pot_full_size(w):
+    say(f"rowmax-pot full-size {w.name}: inputs")
+    inp = synth.workload_inputs(w)
+    sc = scale_of(w.d)
+    tensors = dev_tensors(inp)
+    o, lse = gpu_run(inp, w.causal, sc, POT, tensors)
+    assert np.all(np.isfinite(o)) and np.all(np.isfinite(lse))
+    rng = np.random.default_rng(9)
+    nrows_total = w.B * w.Hq * w.S
+    rows = np.unique(np.concatenate([[0, w.S - 1, nrows_total - 1], rng.integers(0, nrows_total, 9)]))
+    say(f"rowmax-pot full-size {w.name}: oracle on {len(rows)} rows")
+    o_ref, lse_ref = oracle_run(inp, w.causal, sc, POT, rows=rows)
+    assert_close(inp, o.reshape(-1, w.d)[rows], lse.reshape(-1)[rows], o_ref, lse_ref, "rowmax-pot sampled", POT)
+    check_pot_probe(inp, w.S, w.causal, sc, ((w.B - 1, w.Hq - 1, w.S - 40, 40),))
