@@ -44,8 +44,22 @@ def build(extra: list[str] | None = None, verbose: bool = False) -> Path:
         raise RuntimeError(f"hipcc failed ({res.returncode}) building {SRC.name}")
     if verbose:
         sys.stderr.write(res.stderr)
+    check_kernel_stubs(tmp)
     tmp.replace(LIB_PATH)
     return LIB_PATH
+
+
+def check_kernel_stubs(lib: Path) -> None:
+    """Refuse a library whose host side references kernel launch stubs that it
+    does not define (the host compile can drop a kernel's stub without an
+    error; loading the library would then fail)."""
+    res = subprocess.run(["nm", "-D", "--undefined-only", str(lib)], capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"nm failed on {lib.name}: {res.stderr.strip()}")
+    missing = [ln.split()[-1] for ln in res.stdout.splitlines() if "__device_stub__" in ln]
+    if missing:
+        lib.unlink(missing_ok=True)
+        raise RuntimeError(f"{lib.name}: {len(missing)} kernel launch stubs are undefined, e.g. {missing[0]}")
 
 
 if __name__ == "__main__":

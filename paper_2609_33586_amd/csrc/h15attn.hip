@@ -337,34 +337,49 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
   const __amdgpu_buffer_rsrc_t vrsrc = __builtin_amdgcn_make_buffer_rsrc((void*)vg, (short)0, S * C::RB, BUF_DWORD3);
   auto kbuf = [&](int t) { return smem + (t & 1) * C::BUF; };
   auto vbuf = [&](int t) { return smem + (t & 1) * C::BUF + C::TILE; };
-  // waves [W0, W0 + NWS) copy the tile
-  auto stage_k = [&](int t, auto nws, int w0) {
-    constexpr int NWS = decltype(nws)::value;
-    static_assert(C::CHUNKS % (NWS * 64) == 0, "tile/staging mismatch");
-    uint8_t* dst = kbuf(t);
+  // Every wave copies its WAVE_LOADS 1 KB blocks of a tile.  The lane's byte
+  // offset inside the tile is the same for every tile, so it is computed
+  // once; a full tile then adds only the scalar offset of its first row.
+  // The last tile clamps rows beyond S - 1 to the last row (those keys are
+  // masked).  The wave index is scalar, so the LDS destinations (M0) are too.
+  // (The addresses handed to the LDS-copy builtin are named variables: with
+  // an arithmetic expression in those arguments the host side of this
+  // compiler drops the kernels' launch stubs without a diagnostic.)
+  constexpr int WAVE_LOADS = C::CHUNKS / (NW * 64);
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  uint32_t koff_c[WAVE_LOADS], voff_c[WAVE_LOADS];
 #pragma unroll
-    for (int c = 0; c < C::CHUNKS / (NWS * 64); ++c) {
-      const int blk = c * NWS + (wave - w0);  // 1 KB block of the tile
-      const int slot = blk * 64 + lane;
-      const int row = slot / C::NCH, pch = slot % C::NCH;
-      const uint32_t off = (uint32_t)min(t * BC + row, S - 1) * C::RB + ((pch ^ k_swz<DT, D>(row)) << 4);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(krsrc, LDS_PTR(void, dst + blk * 1024), 16, off, 0, 0, 0);
+  for (int c = 0; c < WAVE_LOADS; ++c) {
+    const int slot = (c * NW + wave) * 64 + lane;
+    const int row = slot / C::NCH, pch = slot % C::NCH;
+    koff_c[c] = (uint32_t)(row * C::RB + ((pch ^ k_swz<DT, D>(row)) << 4));
+    voff_c[c] = (uint32_t)(row * C::RB + ((pch ^ v_swz<DT, D>(row)) << 4));
+  }
+  auto stage = [&](int t, uint8_t* dst, const __amdgpu_buffer_rsrc_t& rsrc, const uint32_t (&off_c)[WAVE_LOADS]) {
+    const int key0 = t * BC;
+    if (key0 + BC <= S) {
+      const uint32_t soff = (uint32_t)key0 * C::RB;
+#pragma unroll
+      for (int c = 0; c < WAVE_LOADS; ++c) {
+        const uint32_t voff = off_c[c];
+        uint8_t* ldst = dst + (c * NW + wave_s) * 1024;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, LDS_PTR(void, ldst), 16, voff, soff, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < WAVE_LOADS; ++c) {
+        // the LDS row keeps its slot (and swizzle); only the source row clamps
+        const int row = ((c * NW + wave) * 64 + lane) / C::NCH;
+        const int key = min(key0 + row, S - 1);
+        const uint32_t voff = (uint32_t)(key - key0) * C::RB + (off_c[c] - (uint32_t)row * C::RB);
+        uint8_t* ldst = dst + (c * NW + wave_s) * 1024;
+        const uint32_t soff = (uint32_t)key0 * C::RB;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, LDS_PTR(void, ldst), 16, voff, soff, 0, 0);
+      }
     }
   };
-  auto stage_v = [&](int t, auto nws, int w0) {
-    constexpr int NWS = decltype(nws)::value;
-    static_assert(C::CHUNKS % (NWS * 64) == 0, "tile/staging mismatch");
-    uint8_t* dst = vbuf(t);
-#pragma unroll
-    for (int c = 0; c < C::CHUNKS / (NWS * 64); ++c) {
-      const int blk = c * NWS + (wave - w0);
-      const int slot = blk * 64 + lane;
-      const int row = slot / C::NCH, pch = slot % C::NCH;
-      const uint32_t off = (uint32_t)min(t * BC + row, S - 1) * C::RB + ((pch ^ v_swz<DT, D>(row)) << 4);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(vrsrc, LDS_PTR(void, dst + blk * 1024), 16, off, 0, 0, 0);
-    }
-  };
-  constexpr std::integral_constant<int, NW> ALL_WAVES{};
+  auto stage_k = [&](int t) { stage(t, kbuf(t), krsrc, koff_c); };
+  auto stage_v = [&](int t) { stage(t, vbuf(t), vrsrc, voff_c); };
 
   // ---- running state (this lane's query row; lanes i and i^32 agree on m)
   constexpr int NDB = D / 32;  // 32-column blocks of O^T
@@ -652,11 +667,11 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
   if constexpr (MODE == MODE_ROWMAX_POT) {
     // ---- Rowmax-PoT anchors every weight at the whole-row maximum: a first
     // pass over the key tiles computes it (QK^T and the masked row max only)
-    stage_k(0, ALL_WAVES, 0);
+    stage_k(0);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     for (int t = 0; t < ntiles; ++t) {
-      if (t + 1 < ntiles) stage_k(t + 1, ALL_WAVES, 0);
+      if (t + 1 < ntiles) stage_k(t + 1);
       if (t <= last_act) {
         __builtin_amdgcn_s_setprio(1);
         qk(kbuf(t));
@@ -673,14 +688,14 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
   }
 
   // ---- one tile per step: copy in the next tile, then QK^T, weights, PV
-  stage_k(0, ALL_WAVES, 0);
-  stage_v(0, ALL_WAVES, 0);
+  stage_k(0);
+  stage_v(0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   for (int t = 0; t < ntiles; ++t) {
     if (t + 1 < ntiles) {
-      stage_k(t + 1, ALL_WAVES, 0);
-      stage_v(t + 1, ALL_WAVES, 0);
+      stage_k(t + 1);
+      stage_v(t + 1);
     }
     if (t <= last_act) {
       __builtin_amdgcn_s_setprio(1);
