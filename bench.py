@@ -44,6 +44,12 @@ def parse():
     ap.add_argument("--tau", type=float, default=0.0,
                     help="conditional-rescale threshold in octaves (BF16 workloads only; 0 = running max)")
     ap.add_argument("--tau-per-wave", action="store_true", help="share the rescale decision per 32-row wave")
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the benchmark line: one JSON line per shape of the sequence / dtype / mask / "
+                         "head-dim / head-batch sweep, H15 against the exact control")
+    ap.add_argument("--energy", type=float, default=0.0, metavar="SECONDS",
+                    help="instead of the benchmark line: board energy per forward of H15 and of the exact control, "
+                         "each from a loop of this many seconds with the board power sampled every 100 ms")
     ap.add_argument("--copy-calibration", type=float, default=0.0, metavar="GIB",
                     help="only run a plain device-to-device copy of this many GiB (5 times), "
                          "the reference for scaling HBM byte counters")
@@ -79,6 +85,140 @@ def cpu_baseline(w, inp, scale, target_s):
                       f"FLOPs counted per row as 4*keys*d"}
 
 
+def device_tensors(inp, torch):
+    dev = torch.device("cuda:0")
+    if inp.dtype == 0:
+        return tuple(torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16) for x in (inp.q, inp.k, inp.v))
+    return tuple(torch.from_numpy(x).to(dev).view(torch.float8_e4m3fn) for x in (inp.q, inp.k, inp.v))
+
+
+def time_modes(pkg, torch, q, k, v, inp, causal, scale, modes, warmup=10, rounds=3, per_window=10):
+    """ms per call of each exp mode: alternating rounds of windows timed with
+    HIP events on the launch stream; returns the median window per mode."""
+    B, Hq, S, d = q.shape
+    out = torch.empty((B, Hq, S, d), dtype=torch.bfloat16, device=q.device)
+    lse = torch.empty((B, Hq, S), dtype=torch.float32, device=q.device)
+    st = torch.cuda.current_stream()
+
+    def call(m):
+        pkg.attn_fwd_ex(q, k, v, causal=causal, scale=scale, exp_mode=m, descale=inp.descale, stream=st,
+                        out=out, lse=lse)
+    for m in modes.values():
+        for _ in range(warmup):
+            call(m)
+    torch.cuda.synchronize()
+    res = {name: [] for name in modes}
+    for r in range(rounds):
+        for name in (list(modes) if r % 2 == 0 else list(reversed(list(modes)))):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(st)
+            for _ in range(per_window):
+                call(modes[name])
+            e1.record(st)
+            torch.cuda.synchronize()
+            res[name].append(e0.elapsed_time(e1) / per_window)
+    return {name: float(np.median(v)) for name, v in res.items()}
+
+
+# The sweep of App. B.3's timing matrix on this kernel: FP8 d = 128, 16 heads,
+# batch 1, causal over 1K-32K and non-causal at 8K; BF16 at 8K both masks;
+# d = 64; and other head / batch / GQA splits at 8K.
+SWEEP = ([("fp8", 1, 16, 16, s, 128, True) for s in (1024, 2048, 4096, 8192, 16384, 32768)]
+         + [("fp8", 1, 16, 16, 8192, 128, False), ("bf16", 1, 16, 16, 8192, 128, True),
+            ("bf16", 1, 16, 16, 8192, 128, False), ("fp8", 1, 16, 16, 8192, 64, True),
+            ("fp8", 2, 32, 8, 8192, 128, True), ("fp8", 4, 8, 8, 8192, 128, True),
+            ("fp8", 1, 64, 8, 8192, 128, True), ("fp8", 8, 16, 2, 2048, 128, True)])
+
+
+def sweep():
+    import torch
+    import paper_2609_33586_amd as pkg
+    from paper_2609_33586_amd import synth
+    modes = {"h15": pkg.ATTN_EXP_H15, "exact": pkg.ATTN_EXP_EXACT}
+    for i, (dt, B, Hq, Hkv, S, d, causal) in enumerate(SWEEP):
+        dtype = synth.FP8_E4M3 if dt == "fp8" else synth.BF16
+        inp = synth.make_inputs(B, Hq, Hkv, S, d, dtype, sharp=False, seed=2000 + i)
+        q, k, v = device_tensors(inp, torch)
+        scale = float(np.float32(1.0 / math.sqrt(d)))
+        t = time_modes(pkg, torch, q, k, v, inp, causal, scale, modes)
+        flops = 4.0 * B * Hq * S * S * d * (0.5 if causal else 1.0)
+        print(json.dumps({"dtype": dt, "B": B, "Hq": Hq, "Hkv": Hkv, "S": S, "d": d, "causal": causal,
+                          "h15_us": round(t["h15"] * 1e3, 2), "exact_us": round(t["exact"] * 1e3, 2),
+                          "h15_tflops": round(flops / (t["h15"] * 1e-3) / 1e12, 1),
+                          "exact_tflops": round(flops / (t["exact"] * 1e-3) / 1e12, 1),
+                          "h15_vs_exact_speedup_pct": round(100.0 * (t["exact"] / t["h15"] - 1.0), 2)}), flush=True)
+        del q, k, v
+        torch.cuda.empty_cache()
+
+
+def board_power_watts():
+    """Board power of GPU 0 from the driver's hwmon node (microwatts), or None."""
+    import glob
+    for path in sorted(glob.glob("/sys/class/drm/card*/device/hwmon/hwmon*/power1_input")):
+        try:
+            return int(Path(path).read_text()) / 1e6
+        except (OSError, ValueError):
+            continue
+    return None
+
+
+def energy(seconds: float, workload: str):
+    """Energy per forward (App. B.3 protocol): a loop of `seconds` of forwards in
+    chunks of 50 calls, each followed by a synchronisation, with the board power
+    sampled every 100 ms from 2 s before to 1 s after; E = mean(P) * T / N over
+    the samples taken during the loop, no idle power subtracted."""
+    import threading
+    import torch
+    import paper_2609_33586_amd as pkg
+    from paper_2609_33586_amd import synth
+    if board_power_watts() is None:
+        print(json.dumps({"energy": "no board power reading available"}))
+        return
+    w = synth.WORKLOADS[workload]
+    inp = synth.workload_inputs(w)
+    q, k, v = device_tensors(inp, torch)
+    scale = float(np.float32(1.0 / math.sqrt(w.d)))
+    out = torch.empty((w.B, w.Hq, w.S, w.d), dtype=torch.bfloat16, device=q.device)
+    lse = torch.empty((w.B, w.Hq, w.S), dtype=torch.float32, device=q.device)
+    res = {}
+    for name, mode in (("exact", pkg.ATTN_EXP_EXACT), ("h15", pkg.ATTN_EXP_H15), ("exact_again", pkg.ATTN_EXP_EXACT)):
+        samples, stop = [], threading.Event()
+
+        def sampler():
+            while not stop.is_set():
+                samples.append((time.perf_counter(), board_power_watts()))
+                time.sleep(0.1)
+        for _ in range(20):
+            pkg.attn_fwd_ex(q, k, v, causal=w.causal, scale=scale, exp_mode=mode, descale=inp.descale, out=out, lse=lse)
+        torch.cuda.synchronize()
+        th = threading.Thread(target=sampler, daemon=True)
+        th.start()
+        time.sleep(2.0)
+        t0 = time.perf_counter()
+        n = 0
+        while time.perf_counter() - t0 < seconds:
+            for _ in range(50):
+                pkg.attn_fwd_ex(q, k, v, causal=w.causal, scale=scale, exp_mode=mode, descale=inp.descale, out=out,
+                                lse=lse)
+            torch.cuda.synchronize()
+            n += 50
+        t1 = time.perf_counter()
+        time.sleep(1.0)
+        stop.set()
+        th.join()
+        inside = [p for (ts, p) in samples if t0 <= ts <= t1 and p is not None]
+        pbar = float(np.mean(inside))
+        res[name] = {"calls": n, "seconds": round(t1 - t0, 3), "mean_power_w": round(pbar, 1),
+                     "samples": len(inside), "ms_per_call": round((t1 - t0) / n * 1e3, 4),
+                     "joule_per_forward": round(pbar * (t1 - t0) / n, 5)}
+        print(json.dumps({"energy": name, **res[name]}), flush=True)
+    ex = 0.5 * (res["exact"]["joule_per_forward"] + res["exact_again"]["joule_per_forward"])
+    print(json.dumps({"energy_workload": workload, "h15_joule_per_forward": res["h15"]["joule_per_forward"],
+                      "exact_joule_per_forward_mean_of_two": round(ex, 5),
+                      "h15_vs_exact_energy_pct": round(100.0 * (res["h15"]["joule_per_forward"] / ex - 1.0), 2)}),
+          flush=True)
+
+
 def profiled_traffic(workload: str, mode: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary, when it
     was taken on the kernel source as it is now (else None)."""
@@ -106,6 +246,12 @@ def main():
 
     import torch
 
+    if args.sweep:
+        sweep()
+        return
+    if args.energy > 0:
+        energy(args.energy, args.workload if args.workload != DEFAULT_WORKLOAD else "causal_fp8_b1_h64kv8_s16384_d128_sharp")
+        return
     if args.copy_calibration > 0:
         n = int(args.copy_calibration * (1 << 30))
         src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
