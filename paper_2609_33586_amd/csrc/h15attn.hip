@@ -1,21 +1,24 @@
 // Fused attention forward for gfx950 (MI355X) with the softmax exponential
 // either the hardware exp2 (control) or Rowmax-H15 (Sec. 5.2 Eq. (m-h15),
-// App. B.1 "Implementation"), behind the C ABI declared in h15attn.h.
+// App. B.1 "Implementation") and its finer input roundings S(Q_{2^-k})
+// (App. B.2), or Rowmax-PoT (App. A.6), behind the C ABI declared in
+// h15attn.h.
 //
-// Kernel structure (one workgroup = 8 wave64s = 256 query rows of one head,
-// two waves per SIMD):
+// Kernel structure (one workgroup = 4 wave64s for FP8, 8 for BF16; 32 query
+// rows of one head per wave; two waves per SIMD):
 //   * each wave keeps its 32 query rows of Q in VGPRs as the MFMA B operand;
-//   * key tiles of 128 keys are copied HBM -> LDS with global_load_lds
-//     (no staging registers), double-buffered: the copy of tile t+1 is in
-//     flight while tile t is computed, one barrier per tile;
+//   * key tiles of 128 keys are copied HBM -> LDS with buffer loads that
+//     write LDS directly (no staging registers), double-buffered: the copy
+//     of tile t+1 is in flight while tile t is computed, one barrier per tile;
 //   * scores are computed transposed, S^T = K Q^T, with 32x32 MFMAs (bf16
 //     32x32x16, fp8 32x32x64): each lane owns one query row and 64 of the
 //     tile's 128 keys, so the row max and row sum are in-lane reductions plus
 //     one exchange with lane ^ 32;
-//   * the weights are produced in VALU registers (hardware exp2, or the H15
-//     add/shift), converted to the MFMA operand type and used directly as the
-//     B operand of O^T += V^T P^T: the MFMA contraction index is mapped to
-//     keys so that the S accumulator layout already is the P operand layout;
+//   * the weights are produced in VALU registers (hardware exp2, or the
+//     lattice weights finished two at a time in 16-bit lanes), converted to
+//     the MFMA operand type and used directly as the B operand of
+//     O^T += V^T P^T: the MFMA contraction index is mapped to keys so that
+//     the S accumulator layout already is the P operand layout;
 //   * V is read from LDS with the transposing reads ds_read_b64_tr_b16 (bf16)
 //     and ds_read_b64_tr_b8 (fp8), in the matching key order.
 #include <hip/hip_runtime.h>
@@ -36,6 +39,8 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x2v __attribute__((__vector_size__(2 * sizeof(int))));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short i16x2 __attribute__((ext_vector_type(2)));
 
 #define LDS_PTR(T, p) ((__attribute__((address_space(3))) T*)(p))
 
@@ -60,20 +65,19 @@ constexpr int BUF_DWORD3 = 0x00020000;
 constexpr int SG_MFMA = 0x008;
 constexpr int SG_DS_READ = 0x100;
 constexpr float H15_MAGIC = 12582912.0f;  // 0x4B400000 = 2^23 + 2^22
-constexpr uint32_t MAGIC_BITS = 0x4B400000u;
-constexpr uint32_t ONE_BITS = 0x3F800000u;
-// bits(2^-126) = bits(1.0) - (126 << 23): the bias of the integer-clamp form
-constexpr uint32_t CLAMP_BIAS = 0x00800000u;
+// top half of bits(1.0) in both 16-bit lanes
+constexpr uint32_t ONE_BITS16X2 = 0x3F803F80u;
 
 // Kernel weight modes.  0 is the exact-exp2 control.  The input-rounding
 // family S(Q_{2^-k}) (App. B.2; k = 1 is Rowmax-H15, App. B.1) takes mode
-// 2k - 1 with the clamp in floating point and 2k with the clamp on the
-// integer form (exact only when y + 0x1.8p23 >= 0 for every score).
-// Mode 7 is Rowmax-PoT (App. A.6 Eq. (rowmax-pot)), anchored at the whole-row
-// maximum, BF16 only.
-enum { MODE_EXACT = 0, MODE_H15 = 1, MODE_H15_FASTCLAMP = 2, MODE_ROWMAX_POT = 7 };
+// 2k - 1 with the clamp in FP32 and 2k with the clamp on the rounded integer
+// in 16-bit lanes (exact only when |y| < 2^15 for every score).  Mode 7 is
+// Rowmax-PoT (App. A.6 Eq. (rowmax-pot)), anchored at the whole-row maximum,
+// BF16 only.
+enum { MODE_EXACT = 0, MODE_H15 = 1, MODE_H15_NARROW = 2, MODE_ROWMAX_POT = 7 };
 constexpr int mode_order(int mode) { return (mode + 1) / 2; }
-constexpr bool mode_intclamp(int mode) { return mode != MODE_EXACT && mode != MODE_ROWMAX_POT && mode % 2 == 0; }
+constexpr bool mode_lattice(int mode) { return mode != MODE_EXACT && mode != MODE_ROWMAX_POT; }
+constexpr bool mode_narrow(int mode) { return mode_lattice(mode) && mode % 2 == 0; }
 constexpr int POT_KMAX = 20;  // tail clamp of Rowmax-PoT
 
 struct Params {
@@ -152,22 +156,63 @@ __device__ __forceinline__ void map_block(const Params& p, int L, int& qb, int& 
 // 0x4B400000 (n = RNE(y) lands in the low mantissa bits), left shift by
 // 23 - k (the low k bits of n become the top mantissa bits, the rest the
 // exponent), plus the bits of 1.0, all modulo 2^32.
+//
+// Such a weight has at most k <= 3 mantissa bits, so the low 16 bits of its
+// FP32 pattern are zero and its top 16 bits, (n << (7 - k)) + 0x3F80 modulo
+// 2^16, are its exact BF16 pattern.  The kernel finishes the weights two at
+// a time in the 16-bit lanes of one register: the row sum takes one
+// two-element dot product per pair, and the pair is already a BF16 operand
+// (or one packed conversion away from FP8).
+//
+// sq_pre: the 32-bit value whose low half carries n: bits(max(y, -126 2^k) +
+// magic), or for the narrow clamp bits(y + magic) (the magic's low half is
+// zero, so the low half is n modulo 2^16).
 template <int MODE>
-__device__ __forceinline__ float sq_weight(float s, float ck, float nbk) {
+__device__ __forceinline__ uint32_t sq_pre(float s, float ck, float nbk) {
   constexpr int K = mode_order(MODE);
   const float y = __builtin_fmaf(s, ck, nbk);
-  if constexpr (mode_intclamp(MODE)) {
-    // Same bits as the canonical order when y + magic >= 0 (the launcher only
-    // selects this form when every |y| is provably below 2^22): the clamp
-    // max(n, -126 * 2^k) is taken on n + 126 * 2^k = bits(t) - base with
-    // unsigned saturation, and the bias of the final add absorbs the offset.
-    const float t = y + H15_MAGIC;
-    const uint32_t nc = __builtin_elementwise_sub_sat(__float_as_uint(t), MAGIC_BITS - (126u << K));
-    return __uint_as_float((nc << (23 - K)) + CLAMP_BIAS);
-  } else {
-    const float t = __builtin_fmaxf(y, -126.0f * (float)(1 << K)) + H15_MAGIC;
-    return __uint_as_float((__float_as_uint(t) << (23 - K)) + ONE_BITS);
+  if constexpr (mode_narrow(MODE)) return __float_as_uint(y + H15_MAGIC);
+  else return __float_as_uint(__builtin_fmaxf(y, -126.0f * (float)(1 << K)) + H15_MAGIC);
+}
+
+// The BF16 weights of two keys in one word (u0 in the low lane): the low
+// halves of their sq_pre values, the narrow clamp max(n, -126 2^k) on int16
+// lanes (n is then n itself: the launcher selects the narrow mode only when
+// every |y| is provably below 2^15), and n 2^(7-k) + 0x3F80 per lane modulo
+// 2^16 in one packed multiply-add.
+template <int MODE>
+__device__ __forceinline__ uint32_t sq_pack(uint32_t u0, uint32_t u1) {
+  constexpr int K = mode_order(MODE);
+  uint32_t x = __builtin_amdgcn_perm(u1, u0, 0x05040100u);
+  if constexpr (mode_narrow(MODE)) {
+    constexpr short lo = (short)(-126 * (1 << K));
+    x = __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(i16x2, x), i16x2{lo, lo}));
   }
+  // the multiplier is an inline constant read from its low half in both
+  // lanes (op_sel_hi 0); the addend comes from a scalar register
+  uint32_t r;
+  asm("v_pk_mad_u16 %0, %1, %2, %3 op_sel_hi:[1,0,1]" : "=v"(r) : "v"(x), "n"(1 << (7 - K)), "s"(ONE_BITS16X2));
+  return r;
+}
+
+// sq_pre value of a masked key: its packed weight is +0.  n = 385 * 2^k gives
+// n 2^(7-k) = 0xC080 = -0x3F80 modulo 2^16, and lies above the narrow clamp.
+template <int MODE>
+constexpr uint32_t sq_masked() {
+  return 385u << mode_order(MODE);
+}
+
+// init plus the row sum of a tile's packed weights: one dot product with
+// (1, 1) per word, in two chains.
+__device__ __forceinline__ float pair_sum(const uint32_t (&w)[4][8], float init) {
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  float a[2] = {init, 0.0f};
+#pragma unroll
+  for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+      a[q & 1] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w[kb][q]), ones, a[q & 1], false);
+  return a[0] + a[1];
 }
 
 // Rowmax-PoT weight of one score (App. A.6 Eq. (rowmax-pot)) against the
@@ -451,81 +496,86 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
     }
   };
 
-  // ---- O^T += V^T P^T for the tile whose V sits at vl and whose P is in pb/pf
-  auto pv = [&](const uint8_t* vl) {
+  // ---- O^T += V^T P^T for the tile whose V sits at vl and whose P is in
+  // pb/pf.  The V^T operands are read from LDS PV_AHEAD MFMAs ahead into a
+  // ring of registers: pv_begin(vl) sets the lane's addresses and issues the
+  // first PV_AHEAD reads (early, so that their latency hides behind the
+  // softmax), pv_finish() issues the MFMAs and the remaining reads.  No
+  // other LDS access may come between the two (the waits count reads).
+  //
+  // bf16: lane (d = i32 + 32 db, half g) needs keys 16 ks + 8 (r/4) + 4 g +
+  // r%4 (r = 0..7): two 4-key transposing reads; lane L16 of a 16-lane group
+  // addresses row 4 g + L16/4 (+8), columns 16 (G4%2) + 4 (L16%4) .. +3 of
+  // the 32-column block.  MFMA i covers (db = i / 8, ks = i % 8).
+  // fp8: lane (d = i32 + 32 db, half g) needs, for byte r = 8 rd + e, key
+  // 32 (2 t2 + rd/2) + 16 (rd%2) + 8 (e/4) + 4 g + e%4: four 8-key
+  // transposing reads; lane L16 of a 16-lane group addresses row vrow = base
+  // + 8 (L16/8) + (L16/2)%4, columns d0 + 8 (L16%2) .. +7.  MFMA i covers
+  // (db = i / 2, t2 = i % 2).
+  // In both, the swizzle of the rows a lane reads equals that of vrow, so
+  // only the block db moves the lane's address; the key offset is an
+  // immediate.
+  constexpr int NPV = DT == DT_BF16 ? NDB * 8 : NDB * 2;
+  using VOp = std::conditional_t<DT == DT_BF16, bf16x8, i32x8>;
+  VOp vring[PV_AHEAD + 1];
+  uint32_t vbase[NDB];
+  auto ldv = [&](auto ic) -> VOp {
+    constexpr int i = decltype(ic)::value;
+    if constexpr (DT == DT_BF16) {
+      const i32x2v lo = ds_read_tr16<(16 * (i & 7)) * C::RB>(vbase[i >> 3]);
+      const i32x2v hi = ds_read_tr16<(16 * (i & 7) + 8) * C::RB>(vbase[i >> 3]);
+      return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3));
+    } else {
+      constexpr int t2 = i & 1;
+      const uint32_t a = vbase[i >> 1];
+      const i32x2v p0 = ds_read_tr8<(64 * t2) * C::RB>(a);
+      const i32x2v p1 = ds_read_tr8<(64 * t2 + 16) * C::RB>(a);
+      const i32x2v p2 = ds_read_tr8<(64 * t2 + 32) * C::RB>(a);
+      const i32x2v p3 = ds_read_tr8<(64 * t2 + 48) * C::RB>(a);
+      const i32x4 lo = __builtin_shufflevector(p0, p1, 0, 1, 2, 3);
+      const i32x4 hi = __builtin_shufflevector(p2, p3, 0, 1, 2, 3);
+      return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+  };
+  auto pv_begin = [&](const uint8_t* vl) {
     const uint32_t vla = (uint32_t)(size_t)LDS_PTR(const uint8_t, vl);
     if constexpr (DT == DT_BF16) {
-      // V^T operand: lane (d = i32 + 32 db, half g) needs keys
-      // 16 ks + 8 (r/4) + 4 g + r%4 (r = 0..7): two 4-key transposing reads;
-      // lane L16 of a 16-lane group addresses row 4 g + L16/4 (+8), columns
-      // 16 (G4%2) + 4 (L16%4) .. +3 of the 32-column block.  The swizzle of
-      // those rows equals that of vrow, so only the block db moves the lane's
-      // address; the key offset is an immediate.
       const int vrow = 4 * (G4 >> 1) + (L16 >> 2);
       const int vcolb = (16 * (G4 & 1) + 4 * (L16 & 3)) * 2;
-      uint32_t base[NDB];
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
         const int cb = 64 * db + vcolb;
-        base[db] = vla + vrow * C::RB + (((cb >> 4) ^ v_swz<DT, D>(vrow)) << 4) + (cb & 15);
+        vbase[db] = vla + vrow * C::RB + (((cb >> 4) ^ v_swz<DT, D>(vrow)) << 4) + (cb & 15);
       }
-      // MFMA i covers (db = i / 8, ks = i % 8); V operands run PV_AHEAD ahead
-      auto ldv = [&](auto ic) {
-        constexpr int i = decltype(ic)::value;
-        const i32x2v lo = ds_read_tr16<(16 * (i & 7)) * C::RB>(base[i >> 3]);
-        const i32x2v hi = ds_read_tr16<(16 * (i & 7) + 8) * C::RB>(base[i >> 3]);
-        return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3));
-      };
-      constexpr int NPV = NDB * 8;
-      bf16x8 ring[PV_AHEAD + 1];
-      static_for<0, PV_AHEAD>([&](auto ic) { ring[decltype(ic)::value] = ldv(ic); });
-      static_for<0, NPV>([&](auto ic) {
-        constexpr int i = decltype(ic)::value;
-        // the reads of the PV_AHEAD - 1 later operands may still be in flight
-        lds_wait<2 * (i + PV_AHEAD <= NPV ? PV_AHEAD - 1 : NPV - 1 - i)>(ring[i % (PV_AHEAD + 1)]);
-        oacc[i >> 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ring[i % (PV_AHEAD + 1)], pb[i & 7], oacc[i >> 3], 0, 0, 0);
-        if constexpr (i + PV_AHEAD < NPV)
-          ring[(i + PV_AHEAD) % (PV_AHEAD + 1)] = ldv(std::integral_constant<int, i + PV_AHEAD>{});
-      });
     } else {
-      // V^T operand: lane (d = i32 + 32 db, half g) needs, for byte r = 8 rd + e,
-      // key 32 (2 t2 + rd/2) + 16 (rd%2) + 8 (e/4) + 4 g + e%4: four 8-key
-      // transposing reads; lane L16 of a 16-lane group addresses row
-      // vrow = base + 8 (L16/8) + (L16/2)%4, columns d0 + 8 (L16%2) .. +7.
-      // The swizzle of those rows equals that of vrow.
       const int vrow = 4 * (G4 >> 1) + 8 * (L16 >> 3) + ((L16 >> 1) & 3);
       const int vcol = 16 * (G4 & 1) + 8 * (L16 & 1);
-      uint32_t base[NDB];
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
         const int cb = 32 * db + vcol;
-        base[db] = vla + vrow * C::RB + (((cb >> 4) ^ v_swz<DT, D>(vrow)) << 4) + (cb & 15);
+        vbase[db] = vla + vrow * C::RB + (((cb >> 4) ^ v_swz<DT, D>(vrow)) << 4) + (cb & 15);
       }
-      // MFMA i covers (db = i / 2, t2 = i % 2); V operands run PV_AHEAD ahead
-      auto ldv = [&](auto ic) {
-        constexpr int i = decltype(ic)::value;
-        constexpr int t2 = i & 1;
-        const uint32_t a = base[i >> 1];
-        const i32x2v p0 = ds_read_tr8<(64 * t2) * C::RB>(a);
-        const i32x2v p1 = ds_read_tr8<(64 * t2 + 16) * C::RB>(a);
-        const i32x2v p2 = ds_read_tr8<(64 * t2 + 32) * C::RB>(a);
-        const i32x2v p3 = ds_read_tr8<(64 * t2 + 48) * C::RB>(a);
-        const i32x4 lo = __builtin_shufflevector(p0, p1, 0, 1, 2, 3);
-        const i32x4 hi = __builtin_shufflevector(p2, p3, 0, 1, 2, 3);
-        return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-      };
-      constexpr int NPV = NDB * 2;
-      i32x8 ring[PV_AHEAD + 1];
-      static_for<0, PV_AHEAD>([&](auto ic) { ring[decltype(ic)::value] = ldv(ic); });
-      static_for<0, NPV>([&](auto ic) {
-        constexpr int i = decltype(ic)::value;
-        lds_wait<4 * (i + PV_AHEAD <= NPV ? PV_AHEAD - 1 : NPV - 1 - i)>(ring[i % (PV_AHEAD + 1)]);
-        oacc[i >> 1] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ring[i % (PV_AHEAD + 1)], pf[i & 1],
-                                                                       oacc[i >> 1], 0, 0, 0, 0, 0, 0);
-        if constexpr (i + PV_AHEAD < NPV)
-          ring[(i + PV_AHEAD) % (PV_AHEAD + 1)] = ldv(std::integral_constant<int, i + PV_AHEAD>{});
-      });
     }
+    static_for<0, PV_AHEAD>([&](auto ic) { vring[decltype(ic)::value] = ldv(ic); });
+  };
+  auto pv_finish = [&]() {
+    // reads per operand
+    constexpr int RPO = DT == DT_BF16 ? 2 : 4;
+    static_for<0, NPV>([&](auto ic) {
+      constexpr int i = decltype(ic)::value;
+      // the reads of the PV_AHEAD - 1 later operands may still be in flight
+      lds_wait<RPO * (i + PV_AHEAD <= NPV ? PV_AHEAD - 1 : NPV - 1 - i)>(vring[i % (PV_AHEAD + 1)]);
+      if constexpr (DT == DT_BF16)
+        oacc[i >> 3] =
+            __builtin_amdgcn_mfma_f32_32x32x16_bf16(vring[i % (PV_AHEAD + 1)], pb[i & 7], oacc[i >> 3], 0, 0, 0);
+      else
+        oacc[i >> 1] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vring[i % (PV_AHEAD + 1)], pf[i & 1],
+                                                                       oacc[i >> 1], 0, 0, 0, 0, 0, 0);
+      // each MFMA issues as soon as its operand is in (not after later reads)
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (i + PV_AHEAD < NPV)
+        vring[(i + PV_AHEAD) % (PV_AHEAD + 1)] = ldv(std::integral_constant<int, i + PV_AHEAD>{});
+    });
   };
 
   // ---- masked keys (causal diagonal, ragged tail) of tile t get score -inf;
@@ -582,34 +632,48 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
     }
     const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * p.c1);
     m_run = m_new;
+    // the first V^T operands of this tile load while the weights are computed
+    pv_begin(vbuf(t));
 
-    // weights, in place over the scores
-    if constexpr (MODE != MODE_EXACT) {
+    // weights, in place over the scores (the lattice modes: as BF16 pairs)
+    constexpr bool PACKED = mode_lattice(MODE);
+    uint32_t wpk[4][8];  // word q of block kb: keys 2q, 2q + 1 of sacc[kb]
+    if constexpr (PACKED) {
+      const float nbk = __builtin_fmaf(-m_new, p.ck, (float)(1 << mode_order(MODE)) * off);
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) sacc[kb][j] = __uint_as_float(sq_pre<MODE>(sacc[kb][j], p.ck, nbk));
+      if (need_mask) {
+        // masked keys carry weight 0 (the clamp alone would give 2^-126)
+        const int lim = (CAUSAL ? min(qrow, S - 1) : S - 1) - kt0 - 4 * g;
+        mask_beyond(sacc, lim, __uint_as_float(sq_masked<MODE>()));
+      }
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          wpk[kb][q] = sq_pack<MODE>(__float_as_uint(sacc[kb][2 * q]), __float_as_uint(sacc[kb][2 * q + 1]));
+      l_part = pair_sum(wpk, l_part * alpha);
+    } else {
       if constexpr (MODE == MODE_ROWMAX_POT) {
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
           for (int j = 0; j < 16; ++j) sacc[kb][j] = pot_weight(sacc[kb][j], m_new, p.c1);
+        if (need_mask) {
+          const int lim = (CAUSAL ? min(qrow, S - 1) : S - 1) - kt0 - 4 * g;
+          mask_beyond(sacc, lim, 0.0f);
+        }
       } else {
-        const float nbk = __builtin_fmaf(-m_new, p.ck, (float)(1 << mode_order(MODE)) * off);
+        const float nb1 = __builtin_fmaf(-m_new, p.c1, off);
 #pragma unroll
         for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-          for (int j = 0; j < 16; ++j) sacc[kb][j] = sq_weight<MODE>(sacc[kb][j], p.ck, nbk);
+          for (int j = 0; j < 16; ++j) sacc[kb][j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][j], p.c1, nb1));
       }
-      if (need_mask) {
-        // masked keys carry weight 0 (the clamp alone would give 2^-126)
-        const int lim = (CAUSAL ? min(qrow, S - 1) : S - 1) - kt0 - 4 * g;
-        mask_beyond(sacc, lim, 0.0f);
-      }
-    } else {
-      const float nb1 = __builtin_fmaf(-m_new, p.c1, off);
-#pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-        for (int j = 0; j < 16; ++j) sacc[kb][j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][j], p.c1, nb1));
+      l_part = l_part * alpha + tile_sum(sacc);
     }
-    l_part = l_part * alpha + tile_sum(sacc);
     // skipping the rescale is exact when no row of the wave moved its max
     if (__builtin_amdgcn_ballot_w64(alpha != 1.0f) != 0) {
 #pragma unroll
@@ -621,20 +685,37 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
     // P in the operand type
     if constexpr (DT == DT_BF16) {
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks)
+      for (int ks = 0; ks < 8; ++ks) {
+        if constexpr (PACKED) {
+          const int kb = ks >> 1, q0 = 4 * (ks & 1);
+          pb[ks] = __builtin_bit_cast(bf16x8, u32x4{wpk[kb][q0], wpk[kb][q0 + 1], wpk[kb][q0 + 2], wpk[kb][q0 + 3]});
+        } else {
 #pragma unroll
-        for (int r = 0; r < 8; ++r) pb[ks][r] = (__bf16)sacc[ks >> 1][8 * (ks & 1) + r];
+          for (int r = 0; r < 8; ++r) pb[ks][r] = (__bf16)sacc[ks >> 1][8 * (ks & 1) + r];
+        }
+      }
     } else {
 #pragma unroll
       for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
         for (int w4 = 0; w4 < 8; ++w4) {
           const int kb = 2 * t2 + (w4 >> 2), j0 = 4 * (w4 & 3);
-          // the old value is fully overwritten by the two halves
-          uint32_t word = __float_as_uint(sacc[kb][j0]);
-          word = __builtin_amdgcn_cvt_pk_fp8_f32(sacc[kb][j0], sacc[kb][j0 + 1], word, false);
-          word = __builtin_amdgcn_cvt_pk_fp8_f32(sacc[kb][j0 + 2], sacc[kb][j0 + 3], word, true);
-          pf[t2][w4] = (int)word;
+          if constexpr (PACKED) {
+            // BF16 -> e4m3 with unit scale (the weights are exact in BF16);
+            // the old value is fully overwritten by the two halves
+            i16x2 word = __builtin_bit_cast(i16x2, wpk[kb][j0 / 2]);
+            word = __builtin_amdgcn_cvt_scalef32_pk_fp8_bf16(word, __builtin_bit_cast(bf16x2, wpk[kb][j0 / 2]), 1.0f,
+                                                             false);
+            word = __builtin_amdgcn_cvt_scalef32_pk_fp8_bf16(word, __builtin_bit_cast(bf16x2, wpk[kb][j0 / 2 + 1]),
+                                                             1.0f, true);
+            pf[t2][w4] = __builtin_bit_cast(int, word);
+          } else {
+            // the old value is fully overwritten by the two halves
+            uint32_t word = __float_as_uint(sacc[kb][j0]);
+            word = __builtin_amdgcn_cvt_pk_fp8_f32(sacc[kb][j0], sacc[kb][j0 + 1], word, false);
+            word = __builtin_amdgcn_cvt_pk_fp8_f32(sacc[kb][j0 + 2], sacc[kb][j0 + 3], word, true);
+            pf[t2][w4] = (int)word;
+          }
         }
     }
     if constexpr (PROBE) {
@@ -654,7 +735,8 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
               } else {
                 bits = ((uint32_t)pf[kb >> 1][4 * (kb & 1) + (j >> 2)] >> (8 * (j & 3))) & 0xFFu;
               }
-              p.w_out[rbase + key] = sacc[kb][j];
+              p.w_out[rbase + key] =
+                  PACKED ? __uint_as_float(((wpk[kb][j >> 1] >> (16 * (j & 1))) & 0xFFFFu) << 16) : sacc[kb][j];
               p.p_out[rbase + key] = bits;
             }
           }
@@ -703,7 +785,7 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
       __builtin_amdgcn_s_setprio(0);
       softmax_tile(t);
       __builtin_amdgcn_s_setprio(1);
-      pv(vbuf(t));
+      pv_finish();
       __builtin_amdgcn_s_setprio(0);
     }
     __builtin_amdgcn_s_waitcnt(0);
@@ -767,7 +849,7 @@ hipError_t launch_mode(const Params& p, int mode, hipStream_t st) {
   if constexpr (DT == DT_BF16) {
     if (mode == MODE_ROWMAX_POT) return launch_one<DT, D, CAUSAL, MODE_ROWMAX_POT, PROBE>(p, st);
   }
-  // the integer-clamp forms are only ever chosen for FP8
+  // the narrow-clamp forms are only ever chosen for FP8
   if constexpr (DT == DT_FP8) {
     switch (mode) {
       case 2: return launch_one<DT, D, CAUSAL, 2, PROBE>(p, st);
@@ -807,15 +889,15 @@ int exp_order(int exp_mode) {
 
 // Kernel variant for an ABI exp_mode.  For FP8 every raw logit satisfies
 // |s| <= d * 448^2, so |y| <= 2 ck d 448^2 + 8 * 2^k with ck = 2^k c1; when
-// that is below 2^22 the exponent y + 0x1.8p23 can never go negative and the
-// integer form of the clamp gives exactly the canonical bits.
+// that is below 2^15 the rounded integer n = RNE(y) fits an int16 lane and
+// the clamp can be taken there (the narrow mode).
 int kernel_mode(int dtype, int exp_mode, int d, float ck) {
   if (exp_mode == ATTN_EXP_ROWMAX_POT) return MODE_ROWMAX_POT;
   const int k = exp_order(exp_mode);
   if (k == 0) return MODE_EXACT;
   if (dtype == ATTN_FP8_E4M3) {
     const double ymax = 2.0 * (double)ck * (double)d * 448.0 * 448.0 * (1.0 + 1e-5) + 8.0 * (1 << k);
-    if (ymax < 4194304.0) return 2 * k;
+    if (ymax < 32767.0) return 2 * k;
   }
   return 2 * k - 1;
 }
