@@ -91,7 +91,7 @@ struct Params {
   float tau;          // conditional-rescale threshold (0: the anchor is the running max)
   int tau_wave;       // 1: the anchor decision is shared by the wave's 32 rows
   int nqb;    // query blocks per head
-  int remap;  // XCD-grouped workgroup order is valid for this shape
+  int remap;  // XCD-grouped workgroup order: 0 none, 1 query blocks outermost, 2 KV heads outermost
   // probe target (PROBE instantiations only)
   int pb, ph, prow0, pnrows;
   float* s_out;
@@ -135,10 +135,24 @@ __device__ __forceinline__ void map_block(const Params& p, int L, int& qb, int& 
     // each XCD whole key/value-head groups, so the query heads that read the
     // same K/V share one L2, and walk query blocks longest-first.
     const int x = L & 7, j = L >> 3;
-    const int per = nbh >> 3;
-    const int qi = j / per, loc = j - qi * per;
+    int qi, kvl, gi;
+    if (p.remap == 2) {
+      // one KV head group at a time per XCD: the K/V working set of the
+      // workgroups resident on an XCD is one head's (non-causal, where every
+      // query block reads all of it)
+      const int span = p.nqb * p.G;
+      kvl = j / span;
+      const int r = j - kvl * span;
+      qi = r / p.G;
+      gi = r - qi * p.G;
+    } else {
+      const int per = nbh >> 3;
+      qi = j / per;
+      const int loc = j - qi * per;
+      kvl = loc / p.G;
+      gi = loc - kvl * p.G;
+    }
     qb = p.nqb - 1 - qi;
-    const int kvl = loc / p.G, gi = loc - kvl * p.G;
     const int kvg = kvl * 8 + x;
     b = kvg / p.Hkv;
     h = (kvg - b * p.Hkv) * p.G + gi;
@@ -986,6 +1000,7 @@ int attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse
   Params p;
   const int rc = fill_params(p, q, k, v, o, lse, B, Hq, Hkv, S, d, scale, dtype, exp_mode, opts);
   if (rc != ATTN_OK) return rc;
+  if (p.remap && !causal) p.remap = 2;
   hipStream_t st = opts ? (hipStream_t)opts->stream : nullptr;
   const int mode = kernel_mode(dtype, exp_mode, d, p.ck);
   const hipError_t e = launch_any<false>(p, dtype, d, causal ? 1 : 0, mode, st);
@@ -1004,6 +1019,7 @@ int attn_fwd_probe(const void* q, const void* k, const void* v, void* o, float* 
   Params p;
   const int rc = fill_params(p, q, k, v, o, lse, B, Hq, Hkv, S, d, scale, dtype, exp_mode, opts);
   if (rc != ATTN_OK) return rc;
+  if (p.remap && !causal) p.remap = 2;
   if (!s_out || !w_out || !p_bits_out) return ATTN_EINVAL;
   if (b < 0 || b >= B || h < 0 || h >= Hq || row0 < 0 || nrows < 1 || row0 + nrows > S)
     return ATTN_EINVAL;
