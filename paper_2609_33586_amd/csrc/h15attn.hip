@@ -215,6 +215,9 @@ template <int MODE>
 constexpr uint32_t sq_masked() {
   return 385u << mode_order(MODE);
 }
+// (0x4B3F0000 | sq_masked) = 0x1.8p23 - 2^16 + sq_masked lies below
+// 0x1.8p23 - 2^15 for every mode
+static_assert((385u << 3) < (1u << 15), "the lift stays below every narrow-mode t");
 
 // init plus the row sum of a tile's packed weights: one dot product with
 // (1, 1) per word, in two chains.
@@ -660,8 +663,20 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
         for (int j = 0; j < 16; ++j) sacc[kb][j] = __uint_as_float(sq_pre<MODE>(sacc[kb][j], p.ck, nbk));
       if (need_mask) {
         // masked keys carry weight 0 (the clamp alone would give 2^-126)
-        const int lim = (CAUSAL ? min(qrow, S - 1) : S - 1) - kt0 - 4 * g;
-        mask_beyond(sacc, lim, __uint_as_float(sq_masked<MODE>()));
+        if constexpr (mode_narrow(MODE)) {
+          // their scores are -inf, so t = -inf here; every real t lies in
+          // (0x1.8p23 - 2^15, 0x1.8p23 + 2^7), so one max lifts exactly the
+          // masked keys to a value below all of them whose low half is the
+          // masked-key lane value (v_max3: fmaxf would first canonicalise)
+          const float lift = __uint_as_float(0x4B3F0000u | sq_masked<MODE>());
+#pragma unroll
+          for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) sacc[kb][j] = max3(sacc[kb][j], lift, lift);
+        } else {
+          const int lim = (CAUSAL ? min(qrow, S - 1) : S - 1) - kt0 - 4 * g;
+          mask_beyond(sacc, lim, __uint_as_float(sq_masked<MODE>()));
+        }
       }
 #pragma unroll
       for (int kb = 0; kb < 4; ++kb)
