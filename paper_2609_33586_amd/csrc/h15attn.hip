@@ -400,9 +400,12 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
   auto vbuf = [&](int t) { return smem + (t & 1) * C::BUF + C::TILE; };
   // Every wave copies its WAVE_LOADS 1 KB blocks of a tile.  The lane's byte
   // offset inside the tile is the same for every tile, so it is computed
-  // once; a full tile then adds only the scalar offset of its first row.
-  // The last tile clamps rows beyond S - 1 to the last row (those keys are
-  // masked).  The wave index is scalar, so the LDS destinations (M0) are too.
+  // once; a tile then adds only the scalar offset of its first row.  Rows at
+  // or beyond S (the ragged last tile) lie outside the resource's
+  // num_records = S * RB: the hardware range check (on the sum of both
+  // offsets, per dword) reads them as zero without touching memory, and
+  // those keys are masked.  The wave index is scalar, so the LDS
+  // destinations (M0) are too.
   // (The addresses handed to the LDS-copy builtin are named variables: with
   // an arithmetic expression in those arguments the host side of this
   // compiler drops the kernels' launch stubs without a diagnostic.)
@@ -417,26 +420,12 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
     voff_c[c] = (uint32_t)(row * C::RB + ((pch ^ v_swz<DT, D>(row)) << 4));
   }
   auto stage = [&](int t, uint8_t* dst, const __amdgpu_buffer_rsrc_t& rsrc, const uint32_t (&off_c)[WAVE_LOADS]) {
-    const int key0 = t * BC;
-    if (key0 + BC <= S) {
-      const uint32_t soff = (uint32_t)key0 * C::RB;
+    const uint32_t soff = (uint32_t)(t * BC) * C::RB;
 #pragma unroll
-      for (int c = 0; c < WAVE_LOADS; ++c) {
-        const uint32_t voff = off_c[c];
-        uint8_t* ldst = dst + (c * NW + wave_s) * 1024;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, LDS_PTR(void, ldst), 16, voff, soff, 0, 0);
-      }
-    } else {
-#pragma unroll
-      for (int c = 0; c < WAVE_LOADS; ++c) {
-        // the LDS row keeps its slot (and swizzle); only the source row clamps
-        const int row = ((c * NW + wave) * 64 + lane) / C::NCH;
-        const int key = min(key0 + row, S - 1);
-        const uint32_t voff = (uint32_t)(key - key0) * C::RB + (off_c[c] - (uint32_t)row * C::RB);
-        uint8_t* ldst = dst + (c * NW + wave_s) * 1024;
-        const uint32_t soff = (uint32_t)key0 * C::RB;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, LDS_PTR(void, ldst), 16, voff, soff, 0, 0);
-      }
+    for (int c = 0; c < WAVE_LOADS; ++c) {
+      const uint32_t voff = off_c[c];
+      uint8_t* ldst = dst + (c * NW + wave_s) * 1024;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, LDS_PTR(void, ldst), 16, voff, soff, 0, 0);
     }
   };
   auto stage_k = [&](int t) { stage(t, kbuf(t), krsrc, koff_c); };
