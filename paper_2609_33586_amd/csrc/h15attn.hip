@@ -419,7 +419,8 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
     koff_c[c] = (uint32_t)(row * C::RB + ((pch ^ k_swz<DT, D>(row)) << 4));
     voff_c[c] = (uint32_t)(row * C::RB + ((pch ^ v_swz<DT, D>(row)) << 4));
   }
-  auto stage = [&](int t, uint8_t* dst, const __amdgpu_buffer_rsrc_t& rsrc, const uint32_t (&off_c)[WAVE_LOADS]) {
+  auto stage = [&](int t, uint8_t* dst, const __amdgpu_buffer_rsrc_t& rsrc,
+                   const uint32_t (&off_c)[WAVE_LOADS]) __attribute__((always_inline)) {
     const uint32_t soff = (uint32_t)(t * BC) * C::RB;
 #pragma unroll
     for (int c = 0; c < WAVE_LOADS; ++c) {
@@ -449,7 +450,7 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
   // MFMA i covers (kk = i / 4, kb = i % 4).  Its K operand is read from LDS
   // QK_AHEAD MFMAs in advance into a ring of registers, and the schedule keeps
   // that order, so each MFMA finds its operand loaded.
-  auto qk = [&](const uint8_t* kl) {
+  auto qk = [&](const uint8_t* kl) __attribute__((always_inline)) {
     const int krow_off = i32 * C::RB;
     const int kswz = k_swz<DT, D>(i32);  // == k_swz(kb * 32 + i32)
     constexpr int NQK = 4 * NKQ;
@@ -542,7 +543,7 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
       return __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
     }
   };
-  auto pv_begin = [&](const uint8_t* vl) {
+  auto pv_begin = [&](const uint8_t* vl) __attribute__((always_inline)) {
     const uint32_t vla = (uint32_t)(size_t)LDS_PTR(const uint8_t, vl);
     if constexpr (DT == DT_BF16) {
       const int vrow = 4 * (G4 >> 1) + (L16 >> 2);
@@ -563,7 +564,7 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
     }
     static_for<0, PV_AHEAD>([&](auto ic) { vring[decltype(ic)::value] = ldv(ic); });
   };
-  auto pv_finish = [&]() {
+  auto pv_finish = [&]() __attribute__((always_inline)) {
     // reads per operand
     constexpr int RPO = DT == DT_BF16 ? 2 : 4;
     static_for<0, NPV>([&](auto ic) {
@@ -585,7 +586,7 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
 
   // ---- masked keys (causal diagonal, ragged tail) of tile t get score -inf;
   // returns whether the tile needed masking
-  auto mask_scores = [&](int t) {
+  auto mask_scores = [&](int t) __attribute__((always_inline)) {
     const int kt0 = t * BC;
     const bool need_mask = (CAUSAL && kt0 + BC - 1 > qw0) || (kt0 + BC > S);
     if (need_mask) {
@@ -597,7 +598,7 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
 
   // ---- the scores of tile t become weights, the running state moves, and P
   // is left in pb/pf for the PV product
-  auto softmax_tile = [&](int t) {
+  auto softmax_tile = [&](int t, const uint8_t* vl) __attribute__((always_inline)) {
     const int kt0 = t * BC;
 
     // masking: causal diagonal and the ragged tail only
@@ -638,7 +639,7 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
     const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * p.c1);
     m_run = m_new;
     // the first V^T operands of this tile load while the weights are computed
-    pv_begin(vbuf(t));
+    pv_begin(vl);
 
     // weights, in place over the scores (the lattice modes: as BF16 pairs)
     constexpr bool PACKED = mode_lattice(MODE);
@@ -786,27 +787,36 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
     }
   }
 
-  // ---- one tile per step: copy in the next tile, then QK^T, weights, PV
-  stage_k(0);
-  stage_v(0);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  for (int t = 0; t < ntiles; ++t) {
+  // ---- one tile per step: copy in the next tile, then QK^T, weights, PV.
+  // Steps come in pairs so that each one's LDS buffers are fixed at compile
+  // time and their addresses fold into the reads' immediate offsets.
+  auto step = [&](int t, auto par) __attribute__((always_inline)) {
+    constexpr int P = decltype(par)::value;
+    uint8_t* const kl = smem + P * C::BUF;
+    uint8_t* const vl = kl + C::TILE;
     if (t + 1 < ntiles) {
-      stage_k(t + 1);
-      stage_v(t + 1);
+      stage(t + 1, smem + (1 - P) * C::BUF, krsrc, koff_c);
+      stage(t + 1, smem + (1 - P) * C::BUF + C::TILE, vrsrc, voff_c);
     }
     if (t <= last_act) {
       __builtin_amdgcn_s_setprio(1);
-      qk(kbuf(t));
+      qk(kl);
       __builtin_amdgcn_s_setprio(0);
-      softmax_tile(t);
+      softmax_tile(t, vl);
       __builtin_amdgcn_s_setprio(1);
       pv_finish();
       __builtin_amdgcn_s_setprio(0);
     }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+  };
+  stage_k(0);
+  stage_v(0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  for (int t = 0; t < ntiles; t += 2) {
+    step(t, std::integral_constant<int, 0>{});
+    if (t + 1 < ntiles) step(t + 1, std::integral_constant<int, 1>{});
   }
 
   // ---- epilogue: O = acc / l * v_descale (bf16), LSE
