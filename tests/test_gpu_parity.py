@@ -347,6 +347,27 @@ def test_deterministic_and_every_row_written(dt):
             assert torch.equal(o1.view(torch.int16), o2.view(torch.int16)) and torch.equal(l1, l2)
 
 
+@pytest.mark.parametrize("dt", [BF16, FP8])
+def test_xcd_grouped_orders_write_every_row(dt):
+    # B * Hkv a multiple of 8 turns on the XCD-grouped workgroup orders (query
+    # blocks outermost when causal, KV-head groups outermost when not): every
+    # output row must still be written exactly as without grouping.
+    inp = synth.make_inputs(2, 16, 4, 700, 128, dt, sharp=True, seed=410)
+    sc = scale_of(128)
+    q, k, v = dev_tensors(inp)
+    rows = np.array([0, 699, 700, 5 * 700 + 333, 31 * 700 + 699])
+    for causal in (False, True):
+        say(f"xcd-grouped order dtype={dt} causal={causal}")
+        o = torch.full((2, 16, 700, 128), float("nan"), dtype=torch.bfloat16, device="cuda:0")
+        lse = torch.full((2, 16, 700), float("nan"), dtype=torch.float32, device="cuda:0")
+        pkg.attn_fwd_ex(q, k, v, causal=causal, scale=sc, exp_mode=H15, descale=inp.descale, out=o, lse=lse)
+        torch.cuda.synchronize()
+        assert not torch.isnan(o.float()).any() and not torch.isnan(lse).any()
+        o_ref, lse_ref = oracle_run(inp, causal, sc, H15, rows=rows)
+        assert_close(inp, o.float().cpu().numpy().astype(np.float64).reshape(-1, 128)[rows],
+                     lse.cpu().numpy().astype(np.float64).reshape(-1)[rows], o_ref, lse_ref, "grouped order", H15)
+
+
 EDGE = [(1, 1, 1, 1, 64), (1, 1, 1, 2, 128), (1, 2, 1, 31, 128), (2, 3, 3, 129, 64), (1, 8, 1, 255, 128),
         (3, 4, 2, 257, 128), (1, 16, 2, 1000, 128)]
 
