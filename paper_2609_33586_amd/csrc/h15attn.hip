@@ -225,6 +225,11 @@ static_assert((385u << 3) < (1u << 15), "the lift stays below every narrow-mode 
 
 // init plus the row sum of a tile's packed weights: one dot product with
 // (1, 1) per word, in two chains.
+__device__ __forceinline__ float dot2_ones(uint32_t w, float acc) {
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, acc, false);
+}
+
 __device__ __forceinline__ float pair_sum(const uint32_t (&w)[4][8], float init) {
   const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
   float a[2] = {init, 0.0f};
@@ -450,6 +455,17 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
   // P of the current tile in the operand type (the MFMA B operand of PV)
   bf16x8 pb[DT == DT_BF16 ? 8 : 1];
   i32x8 pf[DT == DT_FP8 ? 2 : 1];
+  // lattice modes: the weights as BF16 pairs, word q of block kb holding keys
+  // 2q and 2q + 1 of sacc[kb]
+  uint32_t wpk[4][8];
+  // FP8 finishes the second half of the tile's P (keys 64..127)
+  // between the PV MFMAs of the first half (MFMA i covers block db = i % NDB
+  // of O^T and key half i / NDB), which do not depend on it, so
+  // that the wave's own VALU work runs while its matrix core is busy; the
+  // row sum's two partial sums (lch) then stay open across the PV product
+  constexpr bool SPLIT = DT == DT_FP8 && MODE != MODE_ROWMAX_POT;
+  float lch[2];
+  float nb1_split = 0.0f;  // exact mode: the exponent bias of the open tile
 
   // ---- S^T = K Q^T for the 128 keys of a tile (4 blocks of 32 keys).
   // MFMA i covers (kk = i / 4, kb = i % 4).  Its K operand is read from LDS
@@ -537,8 +553,8 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
       const i32x2v hi = ds_read_tr16<(16 * (i & 7) + 8) * C::RB>(vbase[i >> 3]);
       return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3));
     } else {
-      constexpr int t2 = i & 1;
-      const uint32_t a = vbase[i >> 1];
+      constexpr int t2 = SPLIT ? i / NDB : i & 1;
+      const uint32_t a = vbase[SPLIT ? i % NDB : i >> 1];
       const i32x2v p0 = ds_read_tr8<(64 * t2) * C::RB>(a);
       const i32x2v p1 = ds_read_tr8<(64 * t2 + 16) * C::RB>(a);
       const i32x2v p2 = ds_read_tr8<(64 * t2 + 32) * C::RB>(a);
@@ -569,6 +585,52 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
     }
     static_for<0, PV_AHEAD>([&](auto ic) { vring[decltype(ic)::value] = ldv(ic); });
   };
+  // ---- split P (FP8 lattice modes): part c (0..3) of the second half packs
+  // words 4 (c % 2) .. +3 of block 2 + c / 2, converts them to P words 2c and
+  // 2c + 1 of pf[1] and adds them to the row sum's chains (the order of
+  // pair_sum, so l is unchanged)
+  auto finish_half = [&](auto cc) __attribute__((always_inline)) {
+    if constexpr (SPLIT && !mode_lattice(MODE)) {
+      // exact mode: part c takes values 8 (c % 2) .. +7 of block 2 + c / 2
+      // through exp2, into P words 2c and 2c + 1, and sums them
+      constexpr int c = decltype(cc)::value;
+      constexpr int kb = 2 + (c >> 1), j0 = 8 * (c & 1);
+#pragma unroll
+      for (int j = j0; j < j0 + 8; ++j)
+        sacc[kb][j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][j], p.c1, nb1_split));
+#pragma unroll
+      for (int w = 0; w < 2; ++w) {
+        const int jw = j0 + 4 * w;
+        uint32_t word = __float_as_uint(sacc[kb][jw]);
+        word = __builtin_amdgcn_cvt_pk_fp8_f32(sacc[kb][jw], sacc[kb][jw + 1], word, false);
+        word = __builtin_amdgcn_cvt_pk_fp8_f32(sacc[kb][jw + 2], sacc[kb][jw + 3], word, true);
+        pf[1][2 * c + w] = (int)word;
+      }
+      const float s8 = ((sacc[kb][j0] + sacc[kb][j0 + 1]) + (sacc[kb][j0 + 2] + sacc[kb][j0 + 3])) +
+                       ((sacc[kb][j0 + 4] + sacc[kb][j0 + 5]) + (sacc[kb][j0 + 6] + sacc[kb][j0 + 7]));
+      if constexpr ((c & 1) == 0) lch[c >> 1] = s8;
+      else lch[c >> 1] += s8;
+      if constexpr (c == 3) l_part += lch[0] + lch[1];
+    } else if constexpr (SPLIT) {
+      constexpr int c = decltype(cc)::value;
+      constexpr int kb = 2 + (c >> 1), q0 = 4 * (c & 1);
+#pragma unroll
+      for (int q = q0; q < q0 + 4; ++q)
+        wpk[kb][q] = sq_pack<MODE>(__float_as_uint(sacc[kb][2 * q]), __float_as_uint(sacc[kb][2 * q + 1]));
+#pragma unroll
+      for (int w = 0; w < 2; ++w) {
+        i16x2 word = __builtin_bit_cast(i16x2, wpk[kb][q0 + 2 * w]);
+        word = __builtin_amdgcn_cvt_scalef32_pk_fp8_bf16(word, __builtin_bit_cast(bf16x2, wpk[kb][q0 + 2 * w]), 1.0f,
+                                                         false);
+        word = __builtin_amdgcn_cvt_scalef32_pk_fp8_bf16(word, __builtin_bit_cast(bf16x2, wpk[kb][q0 + 2 * w + 1]),
+                                                         1.0f, true);
+        pf[1][2 * c + w] = __builtin_bit_cast(int, word);
+      }
+#pragma unroll
+      for (int q = q0; q < q0 + 4; ++q) lch[q & 1] = dot2_ones(wpk[kb][q], lch[q & 1]);
+      if constexpr (c == 3) l_part = lch[0] + lch[1];
+    }
+  };
   auto pv_finish = [&]() __attribute__((always_inline)) {
     // reads per operand
     constexpr int RPO = DT == DT_BF16 ? 2 : 4;
@@ -579,13 +641,22 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
       if constexpr (DT == DT_BF16)
         oacc[i >> 3] =
             __builtin_amdgcn_mfma_f32_32x32x16_bf16(vring[i % (PV_AHEAD + 1)], pb[i & 7], oacc[i >> 3], 0, 0, 0);
-      else
-        oacc[i >> 1] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vring[i % (PV_AHEAD + 1)], pf[i & 1],
-                                                                       oacc[i >> 1], 0, 0, 0, 0, 0, 0);
+      else {
+        constexpr int db = SPLIT ? i % NDB : i >> 1, t2 = SPLIT ? i / NDB : i & 1;
+        static_assert(db < NDB && t2 < 2, "PV operand index");
+        oacc[db] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vring[i % (PV_AHEAD + 1)], pf[t2], oacc[db], 0, 0,
+                                                                   0, 0, 0, 0);
+      }
       // each MFMA issues as soon as its operand is in (not after later reads)
       __builtin_amdgcn_sched_barrier(0);
       if constexpr (i + PV_AHEAD < NPV)
         vring[(i + PV_AHEAD) % (PV_AHEAD + 1)] = ldv(std::integral_constant<int, i + PV_AHEAD>{});
+      if constexpr (SPLIT && i < NDB) {
+        // parts 4i/NDB .. 4(i+1)/NDB - 1 run while MFMA i executes; MFMAs
+        // NDB .. 2 NDB - 1 read what they write
+        static_for<4 * i / NDB, 4 * (i + 1) / NDB>([&](auto cc) { finish_half(cc); });
+        __builtin_amdgcn_sched_barrier(0);
+      }
     });
   };
 
@@ -599,6 +670,36 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
       mask_beyond(sacc, lim, -INFINITY);
     }
     return need_mask;
+  };
+
+  // ---- the probe variant writes tile t's weights and P for its probed rows
+  auto probe_weights = [&](int t) __attribute__((always_inline)) {
+    if constexpr (PROBE) {
+      const int kt0 = t * BC;
+      if (b == p.pb && h == p.ph && qrow >= p.prow0 && qrow < p.prow0 + p.pnrows) {
+        const size_t rbase = (size_t)(qrow - p.prow0) * S;
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+            const int key = kt0 + kb * 32 + 8 * (j >> 2) + 4 * g + (j & 3);
+            if (key < S) {
+              uint32_t bits;
+              if constexpr (DT == DT_BF16) {
+                // read the bf16 bits through a 32-bit view of the operand
+                const u32x4 pw = __builtin_bit_cast(u32x4, pb[2 * kb + (j >> 3)]);
+                bits = (pw[(j & 7) >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+              } else {
+                bits = ((uint32_t)pf[kb >> 1][4 * (kb & 1) + (j >> 2)] >> (8 * (j & 3))) & 0xFFu;
+              }
+              p.w_out[rbase + key] =
+                  mode_lattice(MODE) ? __uint_as_float(((wpk[kb][j >> 1] >> (16 * (j & 1))) & 0xFFFFu) << 16)
+                                     : sacc[kb][j];
+              p.p_out[rbase + key] = bits;
+            }
+          }
+      }
+    }
   };
 
   // ---- the scores of tile t become weights, the running state moves, and P
@@ -648,7 +749,6 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
 
     // weights, in place over the scores (the lattice modes: as BF16 pairs)
     constexpr bool PACKED = mode_lattice(MODE);
-    uint32_t wpk[4][8];  // word q of block kb: keys 2q, 2q + 1 of sacc[kb]
     if constexpr (PACKED) {
       const float nbk = __builtin_fmaf(-m_new, p.ck, (float)(1 << mode_order(MODE)) * off);
 #pragma unroll
@@ -673,11 +773,21 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
         }
       }
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb)
+      for (int kb = 0; kb < (SPLIT ? 2 : 4); ++kb)
 #pragma unroll
         for (int q = 0; q < 8; ++q)
           wpk[kb][q] = sq_pack<MODE>(__float_as_uint(sacc[kb][2 * q]), __float_as_uint(sacc[kb][2 * q + 1]));
-      l_part = pair_sum(wpk, l_part * alpha);
+      if constexpr (SPLIT) {
+        // the same two chains as pair_sum, continued by finish_half
+        lch[0] = l_part * alpha;
+        lch[1] = 0.0f;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int q = 0; q < 8; ++q) lch[q & 1] = dot2_ones(wpk[kb][q], lch[q & 1]);
+      } else {
+        l_part = pair_sum(wpk, l_part * alpha);
+      }
     } else {
       if constexpr (MODE == MODE_ROWMAX_POT) {
 #pragma unroll
@@ -691,11 +801,24 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
       } else {
         const float nb1 = __builtin_fmaf(-m_new, p.c1, off);
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
+        for (int kb = 0; kb < (SPLIT ? 2 : 4); ++kb)
 #pragma unroll
           for (int j = 0; j < 16; ++j) sacc[kb][j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][j], p.c1, nb1));
+        nb1_split = nb1;
       }
-      l_part = l_part * alpha + tile_sum(sacc);
+      if constexpr (SPLIT) {
+        // keys 0..63 now, 64..127 in finish_half
+        float a[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) a[i] = sacc[0][i] + sacc[1][i];
+#pragma unroll
+        for (int w = 8; w >= 1; w >>= 1)
+#pragma unroll
+          for (int i = 0; i < w; ++i) a[i] = a[i] + a[i + w];
+        l_part = l_part * alpha + a[0];
+      } else {
+        l_part = l_part * alpha + tile_sum(sacc);
+      }
     }
     // skipping the rescale is exact when no row of the wave moved its max
     if (__builtin_amdgcn_ballot_w64(alpha != 1.0f) != 0) {
@@ -719,7 +842,7 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
       }
     } else {
 #pragma unroll
-      for (int t2 = 0; t2 < 2; ++t2)
+      for (int t2 = 0; t2 < (SPLIT ? 1 : 2); ++t2)
 #pragma unroll
         for (int w4 = 0; w4 < 8; ++w4) {
           const int kb = 2 * t2 + (w4 >> 2), j0 = 4 * (w4 & 3);
@@ -741,30 +864,7 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
           }
         }
     }
-    if constexpr (PROBE) {
-      if (probe_row) {
-        const size_t rbase = (size_t)(qrow - p.prow0) * S;
-#pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
-#pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            const int key = kt0 + kb * 32 + 8 * (j >> 2) + 4 * g + (j & 3);
-            if (key < S) {
-              uint32_t bits;
-              if constexpr (DT == DT_BF16) {
-                // read the bf16 bits through a 32-bit view of the operand
-                const u32x4 pw = __builtin_bit_cast(u32x4, pb[2 * kb + (j >> 3)]);
-                bits = (pw[(j & 7) >> 1] >> (16 * (j & 1))) & 0xFFFFu;
-              } else {
-                bits = ((uint32_t)pf[kb >> 1][4 * (kb & 1) + (j >> 2)] >> (8 * (j & 3))) & 0xFFu;
-              }
-              p.w_out[rbase + key] =
-                  PACKED ? __uint_as_float(((wpk[kb][j >> 1] >> (16 * (j & 1))) & 0xFFFFu) << 16) : sacc[kb][j];
-              p.p_out[rbase + key] = bits;
-            }
-          }
-      }
-    }
+    if constexpr (!SPLIT) probe_weights(t);
   };
 
   // last tile holding a valid key for some row of this wave (-1: none)
@@ -811,6 +911,7 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
       __builtin_amdgcn_s_setprio(1);
       pv_finish();
       __builtin_amdgcn_s_setprio(0);
+      if constexpr (SPLIT) probe_weights(t);
     }
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
