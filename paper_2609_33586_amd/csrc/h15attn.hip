@@ -462,9 +462,12 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
   // between the PV MFMAs of the first half (MFMA i covers block db = i % NDB
   // of O^T and key half i / NDB), which do not depend on it, so
   // that the wave's own VALU work runs while its matrix core is busy; the
-  // row sum's two partial sums (lch) then stay open across the PV product
+  // row sum's partial sums then stay open across the PV product (exact
+  // mode: the two halves in lch; lattice modes: eight dot2 chains in lch8,
+  // one per word index, none longer than four)
   constexpr bool SPLIT = DT == DT_FP8 && MODE != MODE_ROWMAX_POT;
   float lch[2];
+  float lch8[8];
   float nb1_split = 0.0f;  // exact mode: the exponent bias of the open tile
 
   // ---- S^T = K Q^T for the 128 keys of a tile (4 blocks of 32 keys).
@@ -587,8 +590,7 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
   };
   // ---- split P (FP8 lattice modes): part c (0..3) of the second half packs
   // words 4 (c % 2) .. +3 of block 2 + c / 2, converts them to P words 2c and
-  // 2c + 1 of pf[1] and adds them to the row sum's chains (the order of
-  // pair_sum, so l is unchanged)
+  // 2c + 1 of pf[1] and adds them to the row sum's chains
   auto finish_half = [&](auto cc) __attribute__((always_inline)) {
     if constexpr (SPLIT && !mode_lattice(MODE)) {
       // exact mode: part c takes values 8 (c % 2) .. +7 of block 2 + c / 2
@@ -627,8 +629,9 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
         pf[1][2 * c + w] = __builtin_bit_cast(int, word);
       }
 #pragma unroll
-      for (int q = q0; q < q0 + 4; ++q) lch[q & 1] = dot2_ones(wpk[kb][q], lch[q & 1]);
-      if constexpr (c == 3) l_part = lch[0] + lch[1];
+      for (int q = q0; q < q0 + 4; ++q) lch8[q] = dot2_ones(wpk[kb][q], lch8[q]);
+      if constexpr (c == 3)
+        l_part += ((lch8[0] + lch8[1]) + (lch8[2] + lch8[3])) + ((lch8[4] + lch8[5]) + (lch8[6] + lch8[7]));
     }
   };
   auto pv_finish = [&]() __attribute__((always_inline)) {
@@ -778,13 +781,10 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
         for (int q = 0; q < 8; ++q)
           wpk[kb][q] = sq_pack<MODE>(__float_as_uint(sacc[kb][2 * q]), __float_as_uint(sacc[kb][2 * q + 1]));
       if constexpr (SPLIT) {
-        // the same two chains as pair_sum, continued by finish_half
-        lch[0] = l_part * alpha;
-        lch[1] = 0.0f;
+        // eight chains, continued by finish_half
+        l_part = l_part * alpha;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-          for (int q = 0; q < 8; ++q) lch[q & 1] = dot2_ones(wpk[kb][q], lch[q & 1]);
+        for (int q = 0; q < 8; ++q) lch8[q] = dot2_ones(wpk[1][q], dot2_ones(wpk[0][q], 0.0f));
       } else {
         l_part = pair_sum(wpk, l_part * alpha);
       }
