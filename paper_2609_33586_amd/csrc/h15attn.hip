@@ -20,7 +20,10 @@
 //     O^T += V^T P^T: the MFMA contraction index is mapped to keys so that
 //     the S accumulator layout already is the P operand layout;
 //   * V is read from LDS with the transposing reads ds_read_b64_tr_b16 (bf16)
-//     and ds_read_b64_tr_b8 (fp8), in the matching key order.
+//     and ds_read_b64_tr_b8 (fp8), in the matching key order;
+//   * at fp8 the PV MFMAs over the tile's first 64 keys go first, and the
+//     weights of the other 64 are finished between them (split P), so that
+//     a wave's VALU work overlaps its own matrix-core work.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
