@@ -323,6 +323,18 @@ __device__ __forceinline__ void lds_wait(T& x) {
 // Tree reductions over a lane's 64 scores (short dependency chains).  The
 // maximum is taken with v_max3_f32 directly: fmaxf on matrix-core results
 // would first canonicalize every input (one extra instruction per score).
+// The compiler does not see into the asm, so it inserts no wait states for
+// it: a max3 must not read an MFMA result while that MFMA may still be in
+// the matrix core.  tile_max runs after the whole QK^T sequence: a block
+// written by an earlier MFMA is first read 16-18 instructions after it, with
+// at least three more MFMAs issued in between (the matrix core runs them in
+// order, 32-64 cycles each), and the last MFMA's block is first read 28 or
+// more instructions after it issued (checked on the generated code of the
+// fp8 and bf16 kernels, d = 64 and 128, causal and not).  (Reading
+// a block right after its MFMA, interleaved with the later ones, was
+// measured to return stale values; the IEEE maximum builtin, which the
+// compiler does guard, reorders the V-operand reads and costs 3.5% at
+// non-causal FP8.)
 __device__ __forceinline__ float max3(float a, float b, float c) {
   float r;
   asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
