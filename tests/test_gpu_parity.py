@@ -184,6 +184,19 @@ def test_probe_weights_bit_exact(dt, causal, mode):
     check_probe(inp, S, d, dt, causal, mode, scale_of(d), ((0, 0, 0, 40), (0, 3, 250, 40), (0, 2, S - 37, 37)))
 
 
+@pytest.mark.parametrize("S", [576, 610])
+@pytest.mark.parametrize("dt", [BF16, FP8])
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("mode", ALL_MODES)
+def test_probe_ragged_tail_across_key_halves(S, dt, causal, mode):
+    # The last key tile ends exactly at its 64-key half (S = 576) or inside
+    # the second half (S = 610, 98 keys): at fp8 the kernel finishes the two
+    # halves of a tile's weights at different points of the PV product.
+    d = 128
+    inp = synth.make_inputs(1, 4, 2, S, d, dt, sharp=True, seed=700 + S)
+    check_probe(inp, S, d, dt, causal, mode, scale_of(d), ((0, 1, S - 70, 70), (0, 2, 100, 30)))
+
+
 @pytest.mark.parametrize("side", ["below", "above"])
 @pytest.mark.parametrize("mode", APPROX)
 def test_fp8_saturated_logits_at_the_narrow_clamp_limit(side, mode):
