@@ -368,8 +368,12 @@ __device__ __forceinline__ float tile_sum(const f32x16 (&v)[4]) {
   return a[0];
 }
 
+// Two waves per SIMD, three for fp8 at d = 64 (163 VGPRs, 32 KB of LDS per
+// workgroup: three workgroups fit a CU, and the third wave hides more of the
+// VALU latency in that VALU-bound case).
 template <int DT, int D, bool CAUSAL, int MODE, bool PROBE>
-__global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_fwd_kernel(Params p) {
+__global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, (DT == DT_FP8 && D == 64) ? 3 : 2))) void
+attn_fwd_kernel(Params p) {
   using C = Cfg<DT, D>;
   constexpr int NW = C::NW, BR = C::BR;
   // K and V tiles, each double-buffered
