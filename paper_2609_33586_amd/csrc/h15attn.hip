@@ -5,7 +5,7 @@
 // h15attn.h.
 //
 // Kernel structure (one workgroup = 4 wave64s for FP8, 8 for BF16; 32 query
-// rows of one head per wave; two waves per SIMD):
+// rows of one head per wave; two waves per SIMD, three for FP8 at d = 64):
 //   * each wave keeps its 32 query rows of Q in VGPRs as the MFMA B operand;
 //   * key tiles of 128 keys are copied HBM -> LDS with buffer loads that
 //     write LDS directly (no staging registers), double-buffered: the copy
