@@ -197,6 +197,29 @@ def test_probe_ragged_tail_across_key_halves(S, dt, causal, mode):
     check_probe(inp, S, d, dt, causal, mode, scale_of(d), ((0, 1, S - 70, 70), (0, 2, 100, 30)))
 
 
+@pytest.mark.parametrize("mode", ALL_MODES)
+@pytest.mark.parametrize("dt,d", [(BF16, 64), (BF16, 128), (FP8, 64), (FP8, 128)])
+@pytest.mark.parametrize("causal", [False, True])
+def test_equal_logits_closed_form(mode, dt, d, causal):
+    # K = 0 makes every logit 0: each visible key gets the same weight (2^off
+    # in every mode, exact at the anchor), so O is the plain mean of the
+    # visible V rows and LSE = ln(number of visible keys).  No oracle needed.
+    S = 300
+    inp = synth.make_inputs(1, 4, 2, S, d, dt, sharp=False, seed=900 + d)
+    inp.k[...] = 0
+    o, lse = gpu_run(inp, causal, scale_of(d), mode)
+    vdec = synth.bf16_decode(inp.v) if dt == BF16 else synth.e4m3_decode(inp.v) * inp.descale[2]
+    vdec = vdec.astype(np.float64)
+    G = 2
+    cnt = np.arange(1, S + 1, dtype=np.float64) if causal else np.full(S, float(S))
+    for h in range(4):
+        vh = vdec[0, h // G]
+        mean = np.cumsum(vh, axis=0) / cnt[:, None] if causal else np.broadcast_to(vh.mean(axis=0), vh.shape)
+        assert np.max(np.abs(o[0, h] - mean)) <= TOL[dt] * vmax(inp), f"head {h}"
+        dl = np.abs(lse[0, h] - np.log(cnt)) - 4.0 * np.spacing(np.log(cnt).astype(np.float32))
+        assert np.max(dl) <= 1e-5, f"head {h}"
+
+
 @pytest.mark.parametrize("side", ["below", "above"])
 @pytest.mark.parametrize("mode", APPROX)
 def test_fp8_saturated_logits_at_the_narrow_clamp_limit(side, mode):
