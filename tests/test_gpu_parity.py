@@ -220,6 +220,41 @@ def test_equal_logits_closed_form(mode, dt, d, causal):
         assert np.max(dl) <= 1e-5, f"head {h}"
 
 
+@pytest.mark.parametrize("mode", ALL_MODES)
+@pytest.mark.parametrize("dt,d", [(BF16, 64), (BF16, 128), (FP8, 64), (FP8, 128)])
+@pytest.mark.parametrize("causal", [False, True])
+def test_dominant_key_closed_form(mode, dt, d, causal):
+    # K = 12 Q (MHA): each row's own key outscores every other by at least 40
+    # octaves (83 at d = 128), so every other weight is below 2^-40 of it; O is
+    # the row's own V row and LSE its own scaled logit.  No oracle needed.
+    S = 300
+    base = synth.make_inputs(1, 2, 2, S, d, dt, sharp=False, seed=950 + d)
+    qdec = (synth.bf16_decode(base.q) if dt == BF16 else synth.e4m3_decode(base.q) * base.descale[0])
+    kf = (12.0 * qdec).astype(np.float32)
+    if dt == BF16:
+        inp = synth.Inputs(base.q, synth.bf16_bits(kf), base.v, (1.0, 1.0, 1.0), BF16)
+    else:
+        kc, ks = synth.quantize_e4m3(kf)
+        inp = synth.Inputs(base.q, kc, base.v, (base.descale[0], ks, base.descale[2]), dt)
+    o, lse = gpu_run(inp, causal, scale_of(d), mode)
+    qd = qdec.astype(np.float64)
+    kd = (synth.bf16_decode(inp.k) if dt == BF16 else synth.e4m3_decode(inp.k) * inp.descale[1]).astype(np.float64)
+    vd = (synth.bf16_decode(inp.v) if dt == BF16 else synth.e4m3_decode(inp.v) * inp.descale[2]).astype(np.float64)
+    sc = scale_of(d)
+    for h in range(2):
+        logits = qd[0, h] @ kd[0, h].T
+        if causal:
+            logits = np.where(np.tril(np.ones((S, S), bool)), logits, -np.inf)
+        assert np.all(np.argmax(logits, axis=1) == np.arange(S))
+        assert np.max(np.abs(o[0, h] - vd[0, h])) <= TOL[dt] * vmax(inp), f"head {h}"
+        lse_ref = sc * np.diagonal(logits)
+        # the logit's own accuracy: fp32 sums at BF16; the FP8 matrix core's
+        # accumulation agrees to about 2^-13 of sum |q k|, which here (all
+        # products positive) is 2^-13 of the logit itself
+        rel = 2.0 ** -12 if dt == FP8 else 1e-5
+        assert np.all(np.abs(lse[0, h] - lse_ref) <= rel * np.abs(lse_ref) + 1e-5), f"head {h}"
+
+
 @pytest.mark.parametrize("side", ["below", "above"])
 @pytest.mark.parametrize("mode", APPROX)
 def test_fp8_saturated_logits_at_the_narrow_clamp_limit(side, mode):
