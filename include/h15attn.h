@@ -21,7 +21,7 @@
  *                   k = 2 and k = 3 (App. B.2 "Exponential-map ablation";
  *                   Rowmax-H15 is k = 1): Q_{2^-k}(x) = 2^-k RNE(2^k x),
  *                   S(q) = 2^floor(q) (1 + q - floor(q)) (App. B.1), realised
- *                   as the H15 sequence with 2^k in place of the doubling:
+ *                   as the H15 sequence, the input scaled by 2^k, not 2:
  *                   y = fma(s, ck, fma(-m, ck, 2^k off)), ck = 2^k c1,
  *                   y = max(y, -126 * 2^k), t = y + 0x1.8p23f (RNE),
  *                   w = bits^-1((bits(t) << (23 - k)) + bits(1.0f)).
@@ -117,7 +117,9 @@ typedef struct attn_opts {
     int rescale_per_wave;
 } attn_opts;
 
-/* Attention forward on the default stream with unit descales. */
+/* Attention forward on the default stream with unit descales (FP8 operands
+ * are taken at their stored e4m3 values) and rescale threshold 0: the same as
+ * attn_fwd_ex with opts = {1, 1, 1, NULL, 0, 0}. */
 int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq,
              int Hkv, int S, int d, int causal, float scale, int dtype, int exp_mode);
 

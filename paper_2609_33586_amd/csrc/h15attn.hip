@@ -320,21 +320,23 @@ __device__ __forceinline__ void lds_wait(T& x) {
   asm volatile("s_waitcnt lgkmcnt(%1)" : "+v"(x) : "n"(N));
 }
 
+// The scores of a tile are next read by inline asm (the v_max3_f32 tree of
+// tile_max, and the compare/select of the masking), and the compiler inserts
+// no wait states between a matrix-core write and an inline-asm read.  This
+// statement does: it takes the four score blocks as in/out operands, so it
+// comes after the last QK^T MFMA and every later read of the blocks comes
+// after it, and it holds the wave for 24 wait states, more than the 20 that
+// gfx950 requires between a 16-pass XDL write of a VGPR and a VALU read of
+// it (the shorter MFMAs need fewer).  (Reading a block right after its MFMA,
+// with no such wait, was measured to return stale values.)
+__device__ __forceinline__ void settle_scores(f32x16 (&v)[4]) {
+  asm("s_nop 15\n\ts_nop 7" : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]));
+}
+
 // Tree reductions over a lane's 64 scores (short dependency chains).  The
 // maximum is taken with v_max3_f32 directly: fmaxf on matrix-core results
 // would first canonicalize every input (one extra instruction per score).
-// The compiler does not see into the asm, so it inserts no wait states for
-// it: a max3 must not read an MFMA result while that MFMA may still be in
-// the matrix core.  tile_max runs after the whole QK^T sequence: a block
-// written by an earlier MFMA is first read 16-18 instructions after it, with
-// at least three more MFMAs issued in between (the matrix core runs them in
-// order, 32-64 cycles each), and the last MFMA's block is first read 28 or
-// more instructions after it issued (checked on the generated code of the
-// fp8 and bf16 kernels, d = 64 and 128, causal and not).  (Reading
-// a block right after its MFMA, interleaved with the later ones, was
-// measured to return stale values; the IEEE maximum builtin, which the
-// compiler does guard, reorders the V-operand reads and costs 3.5% at
-// non-causal FP8.)
+// Its reads of the scores come after settle_scores.
 __device__ __forceinline__ float max3(float a, float b, float c) {
   float r;
   asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
@@ -900,6 +902,7 @@ attn_fwd_kernel(Params p) {
         __builtin_amdgcn_s_setprio(1);
         qk(kbuf(t));
         __builtin_amdgcn_s_setprio(0);
+        settle_scores(sacc);
         mask_scores(t);
         const float mt = tile_max(sacc);
         float ma, mb;
@@ -926,6 +929,7 @@ attn_fwd_kernel(Params p) {
       __builtin_amdgcn_s_setprio(1);
       qk(kl);
       __builtin_amdgcn_s_setprio(0);
+      settle_scores(sacc);
       softmax_tile(t, vl);
       __builtin_amdgcn_s_setprio(1);
       pv_finish();
@@ -1147,7 +1151,9 @@ int attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse
 
 int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq,
              int Hkv, int S, int d, int causal, float scale, int dtype, int exp_mode) {
-  return attn_fwd_ex(q, k, v, o, lse, B, Hq, Hkv, S, d, causal, scale, dtype, exp_mode, nullptr);
+  // unit descales (FP8 values are taken as stored), default stream, threshold 0
+  const attn_opts unit = {1.0f, 1.0f, 1.0f, nullptr, 0.0f, 0};
+  return attn_fwd_ex(q, k, v, o, lse, B, Hq, Hkv, S, d, causal, scale, dtype, exp_mode, &unit);
 }
 
 int attn_fwd_probe(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq,
