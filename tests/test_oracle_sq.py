@@ -1,7 +1,7 @@
 """Pins of the oracle's finer input-rounding weights S(Q_{2^-k}(x)) (App. B.2,
 "Exponential-map ablation"): Q_{2^-k}(x) = 2^-k RNE(2^k x) fed to the
 unshifted Schraudolph map S(q) = 2^floor(q) (1 + q - floor(q)) of App. B.1,
-realised by the add of 0x4B400000 with 2^k in place of the doubling and a left
+realised by the add of 0x4B400000 on the input scaled by 2^k (not 2) and a left
 shift by 23 - k.  Checked against the paper's own test set for every k it
 lists, exhaustively for the kernel's k = 2, 3, and against closed forms and
 invariants; never against itself."""
@@ -14,9 +14,10 @@ import oracle
 
 
 def paper_test_inputs() -> np.ndarray:
-    """The paper's 2,295,040 inputs in [-126, 0]: 2,000,000 uniform draws, the
-    integers 0 .. -126 and every multiple of 7 * 2^-14 (which include RNE ties
-    for every k)."""
+    """An input set of the size and make-up App. B.2 uses for its bit-level
+    check (2,295,040 values in [-126, 0]): uniform draws, every integer of the
+    range, and the multiples of 7 * 2^-14 in it, which put RNE ties in the set
+    for every k."""
     rng = np.random.default_rng(2609)
     uni = rng.uniform(-126.0, 0.0, 2_000_000).astype(np.float32)
     ints = -np.arange(0, 127, dtype=np.float32)

@@ -105,8 +105,9 @@ def test_group_decision_moves_every_row():
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("group", [1, 32])
 def test_exact_exponential_is_anchor_free(causal, group):
-    # App. B.2: the conditional rescale recovers the exact denominator for an
-    # exact exponential; only the bf16 storage of P remains (2^-9 relative)
+    # App. B.2: with an exact exponential the anchor does not matter, so the
+    # conditional rescale gives back the exact denominator; only the bf16
+    # storage of P remains (2^-9 relative)
     inp = synth.make_inputs(1, 2, 1, 200, 16, BF16, sharp=True, seed=33)
     sc = 0.3
     o, lse = oracle.attn(inp.q, inp.k, inp.v, dtype=BF16, causal=causal, scale=sc, mode=oracle.EXACT_TILE, Bc=16,
