@@ -25,6 +25,7 @@ ROOT = Path(__file__).resolve().parent
 sys.path.insert(0, str(ROOT))
 
 DEFAULT_WORKLOAD = "causal_fp8_b2_h32kv8_s8192_d128_sharp"
+NONCAUSAL_WORKLOAD = "noncausal_fp8_b2_h16_s8192_d128"
 # MI355X published dense peaks (TFLOP/s)
 PEAK = {"bf16": 2500.0, "fp8_e4m3": 5000.0}
 
@@ -35,7 +36,10 @@ def parse():
     ap.add_argument("--steps", type=int, default=30)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--rounds", type=int, default=3)
+    ap.add_argument("--window", type=int, default=5,
+                    help="calls per timed window; the windows of the timed variants alternate")
+    ap.add_argument("--no-noncausal", action="store_true",
+                    help="do not time the non-causal FP8 8K H15/exact pair beside the default workload")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU baseline sample time")
     ap.add_argument("--modes", default=None,
@@ -120,6 +124,39 @@ def time_modes(pkg, torch, q, k, v, inp, causal, scale, modes, warmup=10, rounds
     return {name: float(np.median(v)) for name, v in res.items()}
 
 
+def timed_windows(torch, stream, calls, steps, warmup, window):
+    """Time every callable of `calls` (name -> launch function) for exactly
+    `steps` calls after `warmup` untimed ones.  The calls run in windows of
+    `window` back-to-back launches bracketed by HIP events on the launch
+    stream, with a synchronisation before each window; the names take turns
+    window by window, in reversed order every other turn.  Returns
+    {name: [(window ms, calls in the window), ...]}."""
+    for fn in calls.values():
+        for _ in range(warmup):
+            fn()
+    torch.cuda.synchronize()
+    names = list(calls)
+    left = {nm: steps for nm in names}
+    res = {nm: [] for nm in names}
+    turn = 0
+    while any(left.values()):
+        for nm in (names if turn % 2 == 0 else names[::-1]):
+            n = min(window, left[nm])
+            if n == 0:
+                continue
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(n):
+                calls[nm]()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            res[nm].append((e0.elapsed_time(e1), n))
+            left[nm] -= n
+        turn += 1
+    return res
+
+
 # The sweep of App. B.3's timing matrix on this kernel: FP8 d = 128, 16 heads,
 # batch 1, causal over 1K-32K and non-causal at 8K; BF16 at 8K both masks;
 # d = 64; and other head / batch / GQA splits at 8K.
@@ -164,8 +201,8 @@ def board_power_watts():
 
 def energy(seconds: float, workload: str):
     """Energy per forward (App. B.3 protocol): a loop of `seconds` of forwards in
-    chunks of 50 calls, each followed by a synchronisation, with the board power
-    sampled every 100 ms from 2 s before to 1 s after; E = mean(P) * T / N over
+    chunks of 50 calls with a synchronisation after each chunk, the board power
+    read every 100 ms, starting 2 s ahead of the loop and stopping 1 s past it; E = mean(P) * T / N over
     the samples taken during the loop, no idle power subtracted."""
     import threading
     import torch
@@ -287,40 +324,36 @@ def main():
         print("bench.py: --tau applies to BF16 workloads only (FP8 keeps the running max)", file=sys.stderr)
         sys.exit(2)
 
-    def call(mode):
-        pkg.attn_fwd_ex(q, k, v, causal=w.causal, scale=scale, exp_mode=modes[mode], descale=inp.descale,
-                        stream=stream, out=out, lse=lse, tau=args.tau, tau_per_wave=args.tau_per_wave)
+    def fwd(q_, k_, v_, inp_, causal_, mode_, out_, lse_):
+        return lambda: pkg.attn_fwd_ex(q_, k_, v_, causal=causal_, scale=scale, exp_mode=mode_,
+                                       descale=inp_.descale, stream=stream, out=out_, lse=lse_, tau=args.tau,
+                                       tau_per_wave=args.tau_per_wave)
 
-    for mode in want:
-        for _ in range(args.warmup):
-            call(mode)
-    torch.cuda.synchronize()
+    calls = {m: fwd(q, k, v, inp, w.causal, modes[m], out, lse) for m in want}
+    # The paper's largest gain is at non-causal 8K (Sec. 5.3): next to the
+    # default causal workload, the non-causal FP8 8K workload's H15 and exact
+    # control run in the same alternating rounds.
+    nc = None
+    if args.workload == DEFAULT_WORKLOAD and not args.no_noncausal and "h15" in want and "exact" in want:
+        nc = synth.WORKLOADS[NONCAUSAL_WORKLOAD]
+        nc_inp = synth.workload_inputs(nc)
+        nq, nk, nv = device_tensors(nc_inp, torch)
+        nout = torch.empty((nc.B, nc.Hq, nc.S, nc.d), dtype=torch.bfloat16, device=dev)
+        nlse = torch.empty((nc.B, nc.Hq, nc.S), dtype=torch.float32, device=dev)
+        calls["nc_h15"] = fwd(nq, nk, nv, nc_inp, False, pkg.ATTN_EXP_H15, nout, nlse)
+        calls["nc_exact"] = fwd(nq, nk, nv, nc_inp, False, pkg.ATTN_EXP_EXACT, nout, nlse)
 
-    # alternating rounds; every round times a window of each mode with HIP
-    # events on the stream the kernels run on
-    per_round = max(1, args.steps // args.rounds)
-    windows = {m: [] for m in want}
-    counts = {m: 0 for m in want}
-    for r in range(args.rounds):
-        order = want if r % 2 == 0 else list(reversed(want))
-        for mode in order:
-            n = per_round if r < args.rounds - 1 else args.steps - per_round * (args.rounds - 1)
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            torch.cuda.synchronize()
-            e0.record(stream)
-            for _ in range(n):
-                call(mode)
-            e1.record(stream)
-            torch.cuda.synchronize()
-            windows[mode].append((e0.elapsed_time(e1), n))
-            counts[mode] += n
+    windows = timed_windows(torch, stream, calls, args.steps, args.warmup, args.window)
 
-    def ms_per_call(mode):
-        tot = sum(t for t, _ in windows[mode])
-        return tot / counts[mode]
+    def mean_ms(name):
+        return sum(t for t, _ in windows[name]) / sum(n for _, n in windows[name])
+
+    def median_ms(name):
+        return float(np.median([t / n for t, n in windows[name]]))
 
     flops = w.flops()
-    res_ms = {m: ms_per_call(m) for m in want}
+    res_ms = {m: mean_ms(m) for m in want}
+    med_ms = {m: median_ms(m) for m in want}
     tflops = {m: flops / (res_ms[m] * 1e-3) / 1e12 for m in want}
     head = "h15" if "h15" in want else want[0]
     peak = PEAK[dtname]
@@ -333,6 +366,9 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(res_ms[head], 5),
+        "ms_per_step_median_window": round(med_ms[head], 5),
+        "value_estimator": f"mean over all {args.steps} timed calls (windows of {args.window} calls, HIP events "
+                           f"on the launch stream); the median window is reported beside it",
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -345,22 +381,36 @@ def main():
                      "frac": round(achieved / peak, 4), "traffic": profiled_traffic(w.name, head)},
     }
     if "h15" in want and "exact" in want:
-        med = {m: float(np.median([t / n for t, n in windows[m]])) for m in want}
         line["control"] = {
             "exact_ms_per_call": round(res_ms["exact"], 5),
+            "exact_ms_per_call_median_window": round(med_ms["exact"], 5),
             "exact_tflops": round(tflops["exact"], 2),
             "exact_mfma_frac": round(tflops["exact"] / peak, 4),
-            "h15_vs_exact_speedup_pct": round(100.0 * (med["exact"] / med["h15"] - 1.0), 2),
+            "h15_vs_exact_speedup_pct": round(100.0 * (res_ms["exact"] / res_ms["h15"] - 1.0), 2),
+            "h15_vs_exact_speedup_pct_median_window": round(100.0 * (med_ms["exact"] / med_ms["h15"] - 1.0), 2),
             "windows_ms_per_call": {m: [round(t / n, 5) for t, n in windows[m]] for m in want},
+        }
+    if nc is not None:
+        nflops = nc.flops()
+        a, b = mean_ms("nc_h15"), mean_ms("nc_exact")
+        am, bm = median_ms("nc_h15"), median_ms("nc_exact")
+        line["control_noncausal_8k"] = {
+            "workload": nc.name,
+            "h15_ms_per_call": round(a, 5), "h15_ms_per_call_median_window": round(am, 5),
+            "exact_ms_per_call": round(b, 5), "exact_ms_per_call_median_window": round(bm, 5),
+            "h15_tflops": round(nflops / (a * 1e-3) / 1e12, 2),
+            "exact_tflops": round(nflops / (b * 1e-3) / 1e12, 2),
+            "h15_mfma_frac": round(nflops / (a * 1e-3) / 1e12 / PEAK["fp8_e4m3"], 4),
+            "h15_vs_exact_speedup_pct": round(100.0 * (b / a - 1.0), 2),
+            "h15_vs_exact_speedup_pct_median_window": round(100.0 * (bm / am - 1.0), 2),
         }
     variants = [m for m in ("sq4", "sq8", "pot") if m in want]
     if variants and "h15" in want:
         # App. B.2's finer input rounding S(Q_{2^-k}), k = 2, 3, and Rowmax-PoT
         # (App. A.6): same kernel, timed in the same alternating rounds
-        med = {m: float(np.median([t / n for t, n in windows[m]])) for m in want}
         line["weight_variants"] = {
             m: {"ms_per_call": round(res_ms[m], 5), "tflops": round(tflops[m], 2),
-                "vs_h15_pct": round(100.0 * (med["h15"] / med[m] - 1.0), 2)} for m in variants}
+                "vs_h15_pct": round(100.0 * (res_ms["h15"] / res_ms[m] - 1.0), 2)} for m in variants}
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(w, inp, scale, args.cpu_seconds)
     print(json.dumps(line), flush=True)

@@ -60,3 +60,53 @@ def test_committed_traffic_record_is_well_formed():
     for wl, modes in rec["workloads"].items():
         for mode, t in modes.items():
             assert t["hbm_read_bytes"] > 0 and t["hbm_write_bytes"] > 0 and t["kernel_avg_us"] > 0, (wl, mode)
+
+
+class _FakeEvent:
+    clock = [0.0]
+
+    def __init__(self, enable_timing=True):
+        self.t = None
+
+    def record(self, stream=None):
+        self.t = _FakeEvent.clock[0]
+
+    def elapsed_time(self, other):
+        return other.t - self.t
+
+
+class _FakeCuda:
+    Event = _FakeEvent
+
+    @staticmethod
+    def synchronize():
+        pass
+
+
+class _FakeTorch:
+    cuda = _FakeCuda
+
+
+def test_timed_windows_counts_every_call_and_alternates():
+    # Every variant gets exactly `steps` timed calls (after `warmup` untimed
+    # ones) in windows of at most `window` calls, and the variants take turns.
+    log = []
+
+    def make(name, ms):
+        def fn():
+            log.append(name)
+            _FakeEvent.clock[0] += ms
+        return fn
+    calls = {"a": make("a", 1.0), "b": make("b", 2.0), "c": make("c", 3.0)}
+    res = bench.timed_windows(_FakeTorch, None, calls, steps=12, warmup=4, window=5)
+    assert log[:12] == ["a"] * 4 + ["b"] * 4 + ["c"] * 4
+    for name, ms in (("a", 1.0), ("b", 2.0), ("c", 3.0)):
+        assert sum(n for _, n in res[name]) == 12
+        assert [n for _, n in res[name]] == [5, 5, 2]
+        assert all(abs(t - ms * n) < 1e-9 for t, n in res[name])
+    # turn 0: a b c; turn 1: c b a; turn 2: a b c (the last windows hold 2)
+    expect = []
+    for names, n in (("abc", 5), ("cba", 5), ("abc", 2)):
+        for nm in names:
+            expect += [nm] * n
+    assert log[12:] == expect
