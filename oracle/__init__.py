@@ -78,6 +78,15 @@ def lib() -> ctypes.CDLL:
     L.oracle_attn.restype = c_i
     L.oracle_logits_row.argtypes = [c_p, c_p, c_i, c_i, c_i, c_i, c_i, c_i, c_i, c_i, c_i, c_p]
     L.oracle_logits_row.restype = c_i
+    L.oracle_sq_row_exponents_from_logits.argtypes = [c_p, c_i, c_i, c_i, c_f, c_i, c_i, c_i, c_i, c_p, c_p, c_p]
+    L.oracle_sq_row_exponents_from_logits.restype = c_i
+    L.oracle_decode.argtypes = [c_p, c_p, c_p, c_i, c_d, c_d, c_d, c_i, c_i, c_i, c_i, c_i, c_i, c_i, c_i, c_d,
+                                c_i, c_i, c_i, c_p, c_i64, c_p, c_p]
+    L.oracle_decode.restype = c_i
+    L.oracle_decode_row_from_logits.argtypes = [c_p, c_i, c_i, c_f, c_i, c_i, c_i, c_i, c_i, c_p, c_p, c_p]
+    L.oracle_decode_row_from_logits.restype = c_i
+    L.oracle_decode_logits_row.argtypes = [c_p, c_p, c_i, c_i, c_i, c_i, c_i, c_i, c_i, c_i, c_i, c_i, c_i, c_p]
+    L.oracle_decode_logits_row.restype = c_i
     _lib = L
     return L
 
@@ -256,7 +265,7 @@ def attn(q: np.ndarray, k: np.ndarray, v: np.ndarray, *, dtype: int, causal: boo
                            int(bool(causal)), float(scale), int(mode), int(Bc), float(tau), int(tau_group),
                            _ptr(rows_arr), int(nrows), _ptr(o), _ptr(lse))
     if rc != 0:
-        raise ValueError("oracle_attn: invalid arguments")
+        raise ValueError("oracle_attn: out of memory" if rc == -3 else "oracle_attn: invalid arguments")
     if rows is None:
         return o.reshape(B, Hq, S, d), lse.reshape(B, Hq, S)
     return o, lse
@@ -272,4 +281,88 @@ def logits_row(q: np.ndarray, k: np.ndarray, dtype: int, b: int, h: int, i: int)
     rc = lib().oracle_logits_row(_ptr(q), _ptr(k), int(dtype), B, Hq, k.shape[1], S, d, b, h, i, _ptr(out))
     if rc != 0:
         raise ValueError("oracle_logits_row: invalid arguments")
+    return out
+
+
+def row_exponents_from_logits(s: np.ndarray, i: int, causal: bool, c1_: float, dtype: int, Bc: int, k: int = 1,
+                              exact_exp: bool = False):
+    """Per-key exponent arguments of row i from fp32 logits: (y, anchor, W).
+
+    y[j] is the fp32 value key j's weight is taken from (2^k x for the lattice
+    weights, x for the exact exponential, before the clamp), anchor[j] the
+    running max of its tile; masked keys have -inf in both."""
+    s = np.ascontiguousarray(s, dtype=np.float32)
+    S = s.shape[0]
+    y = np.zeros(S, np.float32)
+    a = np.zeros(S, np.float32)
+    w = np.zeros(S, np.float32)
+    rc = lib().oracle_sq_row_exponents_from_logits(_ptr(s), S, int(i), int(bool(causal)), float(c1_), int(dtype),
+                                                   int(Bc), int(bool(exact_exp)), int(k), _ptr(y), _ptr(a), _ptr(w))
+    if rc != 0:
+        raise ValueError("oracle_sq_row_exponents_from_logits: invalid arguments")
+    return y, a, w
+
+
+def decode(q: np.ndarray, k: np.ndarray, v: np.ndarray, *, Sk: int, dtype: int, causal: bool, scale: float,
+           mode: int, split_keys: int, descale=(1.0, 1.0, 1.0), Bc: int = 128, rows: np.ndarray | None = None):
+    """Decode attention over a key/value cache (see oracle_decode in attn_oracle.c).
+
+    q: [B,Hq,Sq,d]; k/v: [B,Hkv,Sk_cap,d] whose first Sk rows per head are the
+    cache.  Query i sees keys j <= Sk - Sq + i when causal.  The keys are cut
+    into parts of split_keys (a multiple of Bc; 0: one part), each running the
+    per-tile recurrence on its own, merged exactly.  Returns (O [nrows, d],
+    LSE [nrows]) or, without rows, [B,Hq,Sq,d] and [B,Hq,Sq]."""
+    want = np.uint16 if dtype == BF16 else np.uint8
+    q = np.ascontiguousarray(q, dtype=want)
+    k = np.ascontiguousarray(k, dtype=want)
+    v = np.ascontiguousarray(v, dtype=want)
+    B, Hq, Sq, d = q.shape
+    Hkv, Sk_cap = k.shape[1], k.shape[2]
+    if k.shape != (B, Hkv, Sk_cap, d) or v.shape != k.shape:
+        raise ValueError("shape mismatch")
+    if rows is None:
+        nrows, rows_arr = B * Hq * Sq, None
+    else:
+        rows_arr = np.ascontiguousarray(rows, dtype=np.int64)
+        nrows = rows_arr.shape[0]
+    o = np.zeros((nrows, d), np.float64)
+    lse = np.zeros(nrows, np.float64)
+    qd, kd, vd = (float(x) for x in descale)
+    rc = lib().oracle_decode(_ptr(q), _ptr(k), _ptr(v), int(dtype), qd, kd, vd, B, Hq, Hkv, Sq, int(Sk), Sk_cap, d,
+                             int(bool(causal)), float(scale), int(mode), int(Bc), int(split_keys), _ptr(rows_arr),
+                             int(nrows), _ptr(o), _ptr(lse))
+    if rc != 0:
+        raise ValueError("oracle_decode: out of memory" if rc == -3 else "oracle_decode: invalid arguments")
+    if rows is None:
+        return o.reshape(B, Hq, Sq, d), lse.reshape(B, Hq, Sq)
+    return o, lse
+
+
+def decode_row_from_logits(s: np.ndarray, jend: int, c1_: float, dtype: int, Bc: int, split_keys: int, k: int = 1,
+                           exact_exp: bool = False):
+    """W, P bits and LSE of one decode row from its fp32 logits (jend visible keys)."""
+    s = np.ascontiguousarray(s, dtype=np.float32)
+    Sk = s.shape[0]
+    w = np.zeros(Sk, np.float32)
+    p = np.zeros(Sk, np.uint32)
+    lse = ctypes.c_double(0.0)
+    rc = lib().oracle_decode_row_from_logits(_ptr(s), Sk, int(jend), float(c1_), int(dtype), int(Bc),
+                                             int(split_keys), int(bool(exact_exp)), int(k), _ptr(w), _ptr(p),
+                                             ctypes.byref(lse))
+    if rc != 0:
+        raise ValueError("oracle_decode_row_from_logits: invalid arguments")
+    return w, p, lse.value
+
+
+def decode_logits_row(q: np.ndarray, k: np.ndarray, dtype: int, Sk: int, b: int, h: int, i: int) -> np.ndarray:
+    """fp32 raw logits of one decode row against the first Sk cache rows."""
+    want = np.uint16 if dtype == BF16 else np.uint8
+    q = np.ascontiguousarray(q, dtype=want)
+    k = np.ascontiguousarray(k, dtype=want)
+    B, Hq, Sq, d = q.shape
+    out = np.zeros(int(Sk), np.float32)
+    rc = lib().oracle_decode_logits_row(_ptr(q), _ptr(k), int(dtype), B, Hq, k.shape[1], Sq, int(Sk), k.shape[2], d,
+                                        int(b), int(h), int(i), _ptr(out))
+    if rc != 0:
+        raise ValueError("oracle_decode_logits_row: invalid arguments")
     return out

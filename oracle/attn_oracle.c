@@ -167,8 +167,8 @@ int64_t oracle_h15_exhaustive(float lo, float hi, int64_t* count)
 /* ---- the S(Q_{2^-k}) family (App. B.2 "Exponential-map ablation") ------ */
 
 /* The realisation that the paper's bit-level test describes: the FP32 add of
- * 0x4B400000 and shift of App. B.1 with 2^k in place of the doubling and a
- * left shift by 23 - k.  y is 2^k x in FP32; the clamp x >= -126 becomes
+ * 0x4B400000 and shift of App. B.1, with the input scaled by 2^k instead of
+ * 2 and the result shifted left by 23 - k.  y is 2^k x in FP32; the clamp x >= -126 becomes
  * y >= -126 * 2^k.  k = 1 is Rowmax-H15.  Valid for 0 <= k <= 22 and
  * |y| < 2^22. */
 float oracle_sq_weight(float y, int k)
@@ -272,12 +272,24 @@ static int grows(float mt, float m, float c1, double tau)
     return g > (float)tau;
 }
 
-/*   move   optional per-tile decisions (1: move the anchor to max(m, mt)),
- *          used for a decision shared by a group of rows; NULL: this row's
- *          own test with tau. */
-static void tiled_row(const float* s, const double* vrows, int S, int d, int jend, float c1,
-                      int off, int Bc, double tau, const uint8_t* move, int dtype, int exact_exp,
-                      int kq, double vd, double* o, double* lse, float* w, uint32_t* p, double* acc)
+/* One pass of the per-tile recurrence over the keys [j0, j1) of a row, its
+ * tiles [j0 + t Bc, j0 + (t+1) Bc) taken in increasing order; keys at or
+ * beyond jend are masked (W = P = 0, never in the max) and the pass stops at
+ * the first tile that starts at or beyond jend.  The running max starts at
+ * -inf.  On return *m_out is the pass's final anchor (-inf when it saw no
+ * valid key), *l_out its running sum and acc[d] its output accumulator, both
+ * relative to that anchor (acc unscaled by vd).
+ *   s      fp32 raw logits of the row, indexed by key
+ *   vrows  decoded V rows, indexed by key ([key][d]; NULL: no accumulation)
+ *   move   optional per-tile decisions (1: move the anchor to max(m, mt)),
+ *          indexed by the pass's tile number, used for a decision shared by a
+ *          group of rows; NULL: this row's own test with tau.
+ * Optional per-key outputs (written for the pass's valid keys only): w, p,
+ * y (the fp32 exponent argument the weight is taken from, before any clamp)
+ * and anchor (the running max the key's tile used). */
+static void tile_pass(const float* s, const double* vrows, int d, int j0, int j1, int jend, float c1,
+                      int off, int Bc, double tau, const uint8_t* move, int dtype, int exact_exp, int kq,
+                      float* m_out, double* l_out, double* acc, float* w, uint32_t* p, float* y, float* anchor)
 {
     /* the input-rounding exponent k: 1 for Rowmax-H15 (c2 = 2 c1, shift 22),
      * 2 or 3 for S(Q_{2^-k}) (2^k c1, shift 23 - k); the scaling by 2^k is exact */
@@ -285,16 +297,12 @@ static void tiled_row(const float* s, const double* vrows, int S, int d, int jen
     float m = -INFINITY;
     double l = 0.0;
     if (acc) for (int c = 0; c < d; c++) acc[c] = 0.0;
-    for (int j = 0; j < S; j++) {
-        if (w) w[j] = 0.0f;
-        if (p) p[j] = 0u;
-    }
-    for (int t0 = 0; t0 < S && t0 < jend; t0 += Bc) {
-        int t1 = t0 + Bc < S ? t0 + Bc : S;
+    for (int t0 = j0; t0 < j1 && t0 < jend; t0 += Bc) {
+        int t1 = t0 + Bc < j1 ? t0 + Bc : j1;
         int v1 = t1 < jend ? t1 : jend;
         float mt = -INFINITY;
         for (int j = t0; j < v1; j++) mt = fmaxf(mt, s[j]);
-        int mv = move ? (m == -INFINITY || move[t0 / Bc]) : grows(mt, m, c1, tau);
+        int mv = move ? (m == -INFINITY || move[(t0 - j0) / Bc]) : grows(mt, m, c1, tau);
         float m_new = mv ? fmaxf(m, mt) : m;
         double alpha = (m == -INFINITY) ? 0.0 : exp2(((double)m - (double)m_new) * (double)c1);
         l *= alpha;
@@ -302,10 +310,14 @@ static void tiled_row(const float* s, const double* vrows, int S, int d, int jen
         float nbk = fmaf(-m_new, ck, (float)((1 << kq) * off));
         float nb1 = fmaf(-m_new, c1, (float)off);
         for (int j = t0; j < v1; j++) {
-            float wj;
-            if (exact_exp) wj = (float)exp2((double)fmaf(s[j], c1, nb1));
-            else if (kq == 1) wj = oracle_h15_weight(fmaf(s[j], ck, nbk));
-            else wj = oracle_sq_weight(fmaf(s[j], ck, nbk), kq);
+            float wj, yj;
+            if (exact_exp) {
+                yj = fmaf(s[j], c1, nb1);
+                wj = (float)exp2((double)yj);
+            } else {
+                yj = fmaf(s[j], ck, nbk);
+                wj = kq == 1 ? oracle_h15_weight(yj) : oracle_sq_weight(yj, kq);
+            }
             uint32_t pb;
             double pv;
             if (dtype == OR_BF16) {
@@ -320,9 +332,33 @@ static void tiled_row(const float* s, const double* vrows, int S, int d, int jen
                 for (int c = 0; c < d; c++) acc[c] += pv * vrows[(size_t)j * d + c];
             if (w) w[j] = wj;
             if (p) p[j] = pb;
+            if (y) y[j] = yj;
+            if (anchor) anchor[j] = m_new;
         }
         m = m_new;
     }
+    *m_out = m;
+    *l_out = l;
+}
+
+/* The whole row as one pass (keys 0 .. S-1, valid below jend >= 1), then
+ * O = acc / l * vd and LSE = ln2 (m c1 + log2 l - off).  Per-key outputs of
+ * masked keys are W = P = 0, y = anchor = -inf. */
+static void tiled_row(const float* s, const double* vrows, int S, int d, int jend, float c1,
+                      int off, int Bc, double tau, const uint8_t* move, int dtype, int exact_exp,
+                      int kq, double vd, double* o, double* lse, float* w, uint32_t* p, double* acc,
+                      float* y, float* anchor)
+{
+    for (int j = 0; j < S; j++) {
+        if (w) w[j] = 0.0f;
+        if (p) p[j] = 0u;
+        if (y) y[j] = -INFINITY;
+        if (anchor) anchor[j] = -INFINITY;
+    }
+    float m;
+    double l;
+    tile_pass(s, vrows, d, 0, S, jend, c1, off, Bc, tau, move, dtype, exact_exp, kq, &m, &l, acc, w, p, y,
+              anchor);
     if (o && acc)
         for (int c = 0; c < d; c++) o[c] = acc[c] / l * vd;
     if (lse) *lse = M_LN2 * ((double)m * (double)c1 + log2(l) - (double)off);
@@ -338,7 +374,7 @@ int oracle_sq_row_from_logits(const float* s, int S, int i, int causal, float c1
     int off = dtype == OR_FP8_E4M3 ? 8 : 0;
     int jend = causal ? i + 1 : S;
     tiled_row(s, NULL, S, 0, jend, c1, off, Bc, tau, NULL, dtype, exact_exp, k, 1.0, NULL, lse_out, w_out,
-              p_out, NULL);
+              p_out, NULL, NULL, NULL);
     return 0;
 }
 
@@ -352,7 +388,26 @@ int oracle_sq_row_from_logits_moves(const float* s, int S, int i, int causal, fl
     int off = dtype == OR_FP8_E4M3 ? 8 : 0;
     int jend = causal ? i + 1 : S;
     tiled_row(s, NULL, S, 0, jend, c1, off, Bc, 0.0, move, dtype, 0, k, 1.0, NULL, lse_out, w_out,
-              p_out, NULL);
+              p_out, NULL, NULL, NULL);
+    return 0;
+}
+
+/* The per-key exponent arguments of one row from given fp32 logits: y[j] is
+ * the fp32 value the weight of key j is taken from (2^k x for the lattice
+ * weights, x for the exact exponential; before the clamp) and anchor[j] the
+ * running max of its tile; masked keys get -inf in both.  w[j] as in
+ * oracle_sq_row_from_logits.  (A test uses them to bound how far a weight
+ * can move when the logits move: a lattice weight changes only where y
+ * crosses a rounding boundary.) */
+int oracle_sq_row_exponents_from_logits(const float* s, int S, int i, int causal, float c1, int dtype,
+                                        int Bc, int exact_exp, int k, float* y_out, float* anchor_out,
+                                        float* w_out)
+{
+    if (S <= 0 || Bc <= 0 || i < 0 || i >= S || k < 1 || k > 3 || !y_out || !anchor_out) return -1;
+    int off = dtype == OR_FP8_E4M3 ? 8 : 0;
+    int jend = causal ? i + 1 : S;
+    tiled_row(s, NULL, S, 0, jend, c1, off, Bc, 0.0, NULL, dtype, exact_exp, k, 1.0, NULL, NULL, w_out,
+              NULL, NULL, y_out, anchor_out);
     return 0;
 }
 
@@ -413,11 +468,15 @@ int oracle_group_moves_from_logits(const float* s, int S, int i0, int i1, int ca
 {
     if (S <= 0 || Bc <= 0 || i0 < 0 || i1 <= i0 || i1 > S || !move) return -1;
     const int n = i1 - i0;
-    float m[n];
+    float* m = malloc(sizeof(float) * (size_t)n);
+    float* mt = malloc(sizeof(float) * (size_t)n);
+    if (!m || !mt) {
+        free(m); free(mt);
+        return -3;
+    }
     for (int r = 0; r < n; r++) m[r] = -INFINITY;
     for (int t = 0; t * Bc < S; t++) {
         int any = 0;
-        float mt[n];
         for (int r = 0; r < n; r++) {
             const int jend = causal ? i0 + r + 1 : S;
             const int t0 = t * Bc, t1 = (t0 + Bc < jend) ? t0 + Bc : jend;
@@ -429,18 +488,23 @@ int oracle_group_moves_from_logits(const float* s, int S, int i0, int i1, int ca
         for (int r = 0; r < n; r++)
             if (m[r] == -INFINITY || any) m[r] = fmaxf(m[r], mt[r]);
     }
+    free(m); free(mt);
     return 0;
 }
 
 /* The same decisions for rows [i0, i1) of head (b, h) of stored operands. */
-static void group_moves(const void* q, const void* k, int dtype, int Hq, int Hkv, int S, int d,
-                        int b, int h, int i0, int i1, int causal, float c1, int Bc, double tau,
-                        uint8_t* move)
+static int group_moves(const void* q, const void* k, int dtype, int Hq, int Hkv, int S, int d,
+                       int b, int h, int i0, int i1, int causal, float c1, int Bc, double tau,
+                       uint8_t* move)
 {
     const int n = i1 - i0, hk = h / (Hq / Hkv);
     const size_t kvoff = ((size_t)b * Hkv + hk) * S * d;
     float* s32 = malloc(sizeof(float) * (size_t)n * S);
     double* qrow = malloc(sizeof(double) * d);
+    if (!s32 || !qrow) {
+        free(s32); free(qrow);
+        return -3;
+    }
     for (int r = 0; r < n; r++) {
         const size_t qoff = (((size_t)b * Hq + h) * S + i0 + r) * d;
         for (int c = 0; c < d; c++) qrow[c] = decode(q, qoff + c, dtype);
@@ -450,8 +514,9 @@ static void group_moves(const void* q, const void* k, int dtype, int Hq, int Hkv
             s32[(size_t)r * S + j] = (float)dot;
         }
     }
-    oracle_group_moves_from_logits(s32, S, i0, i1, causal, c1, Bc, tau, move);
+    const int rc = oracle_group_moves_from_logits(s32, S, i0, i1, causal, c1, Bc, tau, move);
     free(s32); free(qrow);
+    return rc;
 }
 
 /* ---- full attention --------------------------------------------------- */
@@ -468,7 +533,7 @@ static double decode(const void* base, size_t idx, int dtype)
  * (uint8).  Query head h reads key/value head h / (Hq/Hkv).  Causal means
  * query i sees keys j <= i.  o receives nrows x d doubles, lse nrows
  * doubles (natural log of the normaliser of the scaled logits).
- * Returns 0, or -1 on invalid arguments. */
+ * Returns 0, -1 on invalid arguments, or -3 when memory ran out. */
 int oracle_attn(const void* q, const void* k, const void* v, int dtype, double qd, double kd,
                 double vd, int B, int Hq, int Hkv, int S, int d, int causal, double scale, int mode,
                 int Bc, double tau, int tau_group, const int64_t* rows, int64_t nrows, double* o,
@@ -485,8 +550,8 @@ int oracle_attn(const void* q, const void* k, const void* v, int dtype, double q
     const double sigma = scale * qd * kd; /* natural-log scale of a raw logit */
     const float c1 = oracle_c1(scale, qd, kd);
     const int off = dtype == OR_FP8_E4M3 ? 8 : 0;
-    int bad = 0;
-#pragma omp parallel for schedule(dynamic, 4) reduction(| : bad)
+    int bad = 0, nomem = 0;
+#pragma omp parallel for schedule(dynamic, 4) reduction(| : bad, nomem)
     for (int64_t r = 0; r < nrows; r++) {
         int64_t flat = rows ? rows[r] : r;
         if (flat < 0 || flat >= total) { bad = 1; continue; }
@@ -503,6 +568,11 @@ int oracle_attn(const void* q, const void* k, const void* v, int dtype, double q
         double* vrows = malloc(sizeof(double) * (size_t)jend * d);
         double* acc = malloc(sizeof(double) * d);
         float* s32 = malloc(sizeof(float) * S);
+        if (!qrow || !sexact || !vrows || !acc || !s32) {
+            free(qrow); free(sexact); free(vrows); free(acc); free(s32);
+            nomem = 1;
+            continue;
+        }
         for (int c = 0; c < d; c++) qrow[c] = decode(q, qoff + c, dtype);
         for (int j = 0; j < jend; j++) {
             double dot = 0.0;
@@ -542,15 +612,20 @@ int oracle_attn(const void* q, const void* k, const void* v, int dtype, double q
                 const int i0 = i / tau_group * tau_group;
                 const int i1 = i0 + tau_group < S ? i0 + tau_group : S;
                 move = malloc((size_t)(S / tile + 1));
-                group_moves(q, k, dtype, Hq, Hkv, S, d, b, h, i0, i1, causal, c1, tile, tau, move);
+                if (!move || group_moves(q, k, dtype, Hq, Hkv, S, d, b, h, i0, i1, causal, c1, tile, tau,
+                                         move) != 0) {
+                    free(move); free(qrow); free(sexact); free(vrows); free(acc); free(s32);
+                    nomem = 1;
+                    continue;
+                }
             }
             tiled_row(s32, vrows, S, d, jend, c1, off, tile, tau, move, dtype, mode == OR_EXACT_TILE, kq,
-                      vd, orow, lse ? &lse[r] : NULL, NULL, NULL, acc);
+                      vd, orow, lse ? &lse[r] : NULL, NULL, NULL, acc, NULL, NULL);
             free(move);
         }
         free(qrow); free(sexact); free(vrows); free(acc); free(s32);
     }
-    return bad ? -1 : 0;
+    return bad ? -1 : nomem ? -3 : 0;
 }
 
 /* Raw fp32 logits s_ij = fp32(sum_c q_ic k_jc) of one query row (exact fp64
@@ -565,6 +640,176 @@ int oracle_logits_row(const void* q, const void* k, int dtype, int B, int Hq, in
     const size_t qoff = (((size_t)b * Hq + h) * S + i) * d;
     const size_t kvoff = ((size_t)b * Hkv + hk) * S * d;
     for (int j = 0; j < S; j++) {
+        double dot = 0.0;
+        for (int c = 0; c < d; c++)
+            dot += decode(q, qoff + c, dtype) * decode(k, kvoff + (size_t)j * d + c, dtype);
+        s_out[j] = (float)dot;
+    }
+    return 0;
+}
+
+/* ---- decode over a key/value cache ------------------------------------ */
+
+/* The paper states attention for square inputs (App. A.1: one query row per
+ * key position) and leaves decode out of its scope; this is the extension
+ * the library implements.  Sq query rows per head attend to the first Sk
+ * rows of a key/value cache; query position i sees keys j <= Sk - Sq + i
+ * when causal (bottom-right alignment: the last query row sees the whole
+ * cache, and with Sq = Sk this is the square causal mask), every key
+ * otherwise.
+ *
+ * The keys are cut into consecutive parts of split_keys keys (a positive
+ * multiple of Bc; 0 or >= Sk: one part).  Within each part the per-tile
+ * recurrence of App. B.1 / B.2 runs on its own: its tiles start at the
+ * part's first key and its running max starts at -inf, so the weights of a
+ * part are taken relative to the part's own running maxima.  The parts then
+ * merge exactly (the softmax identity, fp64):
+ *     m = max_p m_p,   f_p = 2^(c1 (m_p - m)),
+ *     l = sum_p f_p l_p,   acc = sum_p f_p acc_p,
+ *     O = acc / l * vd,    LSE = ln2 (m c1 + log2 l - off),
+ * parts without a visible key taking no part.  With one part this is the
+ * whole row's recurrence (tiled_row).  EXACT mode is the plain softmax over
+ * the visible keys, which no cut changes. */
+static void decode_row(const float* s32, const double* vrows, int Sk, int d, int jend, float c1, int off,
+                       int Bc, int split_keys, int dtype, int exact_exp, int kq, double vd, double* o,
+                       double* lse, float* w, uint32_t* p, double* acc, double* part_acc)
+{
+    const int part = (split_keys <= 0 || split_keys >= Sk) ? Sk : split_keys;
+    for (int j = 0; j < Sk; j++) {
+        if (w) w[j] = 0.0f;
+        if (p) p[j] = 0u;
+    }
+    /* the merged maximum first, then every part rescaled to it */
+    const int nparts = (Sk + part - 1) / part;
+    float m = -INFINITY;
+    for (int j = 0; j < jend; j++) m = fmaxf(m, s32[j]);
+    double l = 0.0;
+    if (acc) for (int c = 0; c < d; c++) acc[c] = 0.0;
+    for (int pi = 0; pi < nparts; pi++) {
+        const int j0 = pi * part, j1 = j0 + part < Sk ? j0 + part : Sk;
+        if (j0 >= jend) break; /* no visible key in this part or any later one */
+        float mp;
+        double lp;
+        tile_pass(s32, vrows, d, j0, j1, jend, c1, off, Bc, 0.0, NULL, dtype, exact_exp, kq, &mp, &lp,
+                  part_acc, w, p, NULL, NULL);
+        const double f = exp2(((double)mp - (double)m) * (double)c1);
+        l += f * lp;
+        if (acc && part_acc)
+            for (int c = 0; c < d; c++) acc[c] += f * part_acc[c];
+    }
+    if (o && acc)
+        for (int c = 0; c < d; c++) o[c] = acc[c] / l * vd;
+    if (lse) *lse = M_LN2 * ((double)m * (double)c1 + log2(l) - (double)off);
+}
+
+/* Decode attention for the listed rows (flat index (b*Hq + h)*Sq + i), or for
+ * all B*Hq*Sq rows when rows == NULL.  q: [B][Hq][Sq][d]; k, v:
+ * [B][Hkv][Sk_cap][d] of which the first Sk rows of every head are the cache
+ * (bf16 bit patterns or e4m3 codes).  Modes: OR_EXACT, OR_H15_TILE,
+ * OR_SQ4_TILE, OR_SQ8_TILE, OR_EXACT_TILE.  o receives nrows x d doubles, lse
+ * nrows doubles.  Returns 0, -1 on invalid arguments (including
+ * Sq > Sk, Sk > Sk_cap, or a split_keys that is not a multiple of Bc), or -3
+ * when memory ran out. */
+int oracle_decode(const void* q, const void* k, const void* v, int dtype, double qd, double kd, double vd,
+                  int B, int Hq, int Hkv, int Sq, int Sk, int Sk_cap, int d, int causal, double scale,
+                  int mode, int Bc, int split_keys, const int64_t* rows, int64_t nrows, double* o,
+                  double* lse)
+{
+    if (!q || !k || !v || !o || B <= 0 || Hq <= 0 || Hkv <= 0 || Sq <= 0 || Sk <= 0 || d <= 0) return -1;
+    if (Hq % Hkv != 0 || Sq > Sk || Sk > Sk_cap || Bc <= 0 || split_keys < 0 || split_keys % Bc != 0)
+        return -1;
+    if (dtype != OR_BF16 && dtype != OR_FP8_E4M3) return -1;
+    if (mode != OR_EXACT && mode != OR_H15_TILE && mode != OR_SQ4_TILE && mode != OR_SQ8_TILE &&
+        mode != OR_EXACT_TILE)
+        return -1;
+    const int64_t total = (int64_t)B * Hq * Sq;
+    if (!rows) nrows = total;
+    const int group = Hq / Hkv;
+    const double sigma = scale * qd * kd;
+    const float c1 = oracle_c1(scale, qd, kd);
+    const int off = dtype == OR_FP8_E4M3 ? 8 : 0;
+    const int kq = mode == OR_SQ4_TILE ? 2 : mode == OR_SQ8_TILE ? 3 : 1;
+    int bad = 0, nomem = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : bad, nomem)
+    for (int64_t r = 0; r < nrows; r++) {
+        int64_t flat = rows ? rows[r] : r;
+        if (flat < 0 || flat >= total) { bad = 1; continue; }
+        const int i = (int)(flat % Sq);
+        const int h = (int)((flat / Sq) % Hq);
+        const int b = (int)(flat / ((int64_t)Sq * Hq));
+        const int hk = h / group;
+        const size_t qoff = (((size_t)b * Hq + h) * Sq + i) * d;
+        const size_t kvoff = ((size_t)b * Hkv + hk) * (size_t)Sk_cap * d;
+        const int jend = causal ? Sk - Sq + i + 1 : Sk;
+        double* qrow = malloc(sizeof(double) * d);
+        double* sexact = malloc(sizeof(double) * Sk);
+        double* vrows = malloc(sizeof(double) * (size_t)jend * d);
+        double* acc = malloc(sizeof(double) * d);
+        double* part_acc = malloc(sizeof(double) * d);
+        float* s32 = malloc(sizeof(float) * Sk);
+        if (!qrow || !sexact || !vrows || !acc || !part_acc || !s32) {
+            free(qrow); free(sexact); free(vrows); free(acc); free(part_acc); free(s32);
+            nomem = 1;
+            continue;
+        }
+        for (int c = 0; c < d; c++) qrow[c] = decode(q, qoff + c, dtype);
+        for (int j = 0; j < jend; j++) {
+            double dot = 0.0;
+            for (int c = 0; c < d; c++) dot += qrow[c] * decode(k, kvoff + (size_t)j * d + c, dtype);
+            sexact[j] = dot;
+            s32[j] = (float)dot;
+            for (int c = 0; c < d; c++) vrows[(size_t)j * d + c] = decode(v, kvoff + (size_t)j * d + c, dtype);
+        }
+        for (int j = jend; j < Sk; j++) s32[j] = 0.0f; /* never read: masked */
+        double* orow = o + (size_t)r * d;
+        if (mode == OR_EXACT) {
+            double smax = -INFINITY;
+            for (int j = 0; j < jend; j++) smax = fmax(smax, sexact[j]);
+            double den = 0.0;
+            for (int c = 0; c < d; c++) acc[c] = 0.0;
+            for (int j = 0; j < jend; j++) {
+                const double wj = exp(-sigma * (smax - sexact[j]));
+                den += wj;
+                for (int c = 0; c < d; c++) acc[c] += wj * vrows[(size_t)j * d + c];
+            }
+            for (int c = 0; c < d; c++) orow[c] = acc[c] / den * vd;
+            if (lse) lse[r] = sigma * smax + log(den);
+        } else {
+            decode_row(s32, vrows, Sk, d, jend, c1, off, Bc, split_keys, dtype, mode == OR_EXACT_TILE, kq, vd,
+                       orow, lse ? &lse[r] : NULL, NULL, NULL, acc, part_acc);
+        }
+        free(qrow); free(sexact); free(vrows); free(acc); free(part_acc); free(s32);
+    }
+    return bad ? -1 : nomem ? -3 : 0;
+}
+
+/* W and P of one decode row from given fp32 logits s[0 .. Sk-1] with the
+ * part semantics of oracle_decode (jend visible keys), and its LSE. */
+int oracle_decode_row_from_logits(const float* s, int Sk, int jend, float c1, int dtype, int Bc,
+                                  int split_keys, int exact_exp, int k, float* w_out, uint32_t* p_out,
+                                  double* lse_out)
+{
+    if (Sk <= 0 || jend < 1 || jend > Sk || Bc <= 0 || split_keys < 0 || split_keys % Bc != 0 || k < 1 ||
+        k > 3)
+        return -1;
+    const int off = dtype == OR_FP8_E4M3 ? 8 : 0;
+    decode_row(s, NULL, Sk, 0, jend, c1, off, Bc, split_keys, dtype, exact_exp, k, 1.0, NULL, lse_out, w_out,
+               p_out, NULL, NULL);
+    return 0;
+}
+
+/* Raw fp32 logits of one decode row (exact fp64 dot products of the stored
+ * operands, rounded once), layouts as in oracle_decode. */
+int oracle_decode_logits_row(const void* q, const void* k, int dtype, int B, int Hq, int Hkv, int Sq, int Sk,
+                             int Sk_cap, int d, int b, int h, int i, float* s_out)
+{
+    if (!q || !k || !s_out || b < 0 || b >= B || h < 0 || h >= Hq || i < 0 || i >= Sq || Hkv <= 0 ||
+        Hq % Hkv || Sk > Sk_cap)
+        return -1;
+    const int hk = h / (Hq / Hkv);
+    const size_t qoff = (((size_t)b * Hq + h) * Sq + i) * d;
+    const size_t kvoff = ((size_t)b * Hkv + hk) * (size_t)Sk_cap * d;
+    for (int j = 0; j < Sk; j++) {
         double dot = 0.0;
         for (int c = 0; c < d; c++)
             dot += decode(q, qoff + c, dtype) * decode(k, kvoff + (size_t)j * d + c, dtype);

@@ -11,7 +11,7 @@ LIB_PATH = HERE / "liboracle.so"
 # No fast-math and no FMA contraction: the FP32 steps must round exactly as
 # written.  -O2 without -march=native so the result is the same on any x86-64.
 CFLAGS = ["-O2", "-std=c11", "-D_GNU_SOURCE", "-fPIC", "-shared", "-fopenmp",
-          "-ffp-contract=off", "-fno-fast-math", "-Wall", "-Wextra"]
+          "-ffp-contract=off", "-fno-fast-math", "-Wall", "-Wextra", "-Wvla"]
 
 
 def build() -> Path:

@@ -345,3 +345,80 @@ def test_rowmax_pot_row_form_matches_fp64_operator():
             w = w.astype(np.float64)
             assert np.max(np.abs(o[0, h, i] - (w @ vdq[0, 0]) / w.sum())) < 1e-12
             assert abs(lse[0, h, i] - lse_row) < 1e-12
+
+
+def exact_tile_prefix_form(s, v, jend, c1, Bc, off, dtype):
+    """The exact-exp2 tile loop written out (diagnostic mode EXACT_TILE): key
+    j in tile t gets W = fp32(2^y), y = fp32(s_j c1 + fp32(-M_t c1 + off)) with
+    M_t the prefix max; PV uses W stored in the operand type (bf16 RNE or e4m3),
+    the row sum W itself; every later rescale is 2^(c1 (M_t - M))."""
+    tiles = [(t0, min(t0 + Bc, jend)) for t0 in range(0, jend, Bc)]
+    m, prefix = -np.inf, []
+    for t0, t1 in tiles:
+        m = max(m, float(np.max(s[t0:t1])))
+        prefix.append(np.float32(m))
+    M = float(prefix[-1])
+    num = np.zeros(v.shape[1])
+    den = 0.0
+    for (t0, t1), Mt in zip(tiles, prefix):
+        nb = round_f32(-Fraction(float(Mt)) * Fraction(float(c1)) + off)
+        for j in range(t0, t1):
+            y = round_f32(Fraction(float(s[j])) * Fraction(float(c1)) + Fraction(float(nb)))
+            w = np.float32(2.0 ** float(y))
+            if dtype == BF16:
+                pv = float(synth.bf16_decode(synth.bf16_bits(np.array([w], np.float32)))[0])
+            else:
+                pv = float(synth.e4m3_decode(synth.e4m3_codes(np.array([w], np.float64)))[0])
+            f = 2.0 ** (float(c1) * (float(Mt) - M))
+            num += pv * f * v[j]
+            den += float(w) * f
+    return num / den, math.log(2) * (M * float(c1) + math.log2(den) - off)
+
+
+@pytest.mark.parametrize("dtype", [BF16, FP8])
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("Bc", [1, 16, 1000])
+def test_exact_tile_matches_prefix_max_form(dtype, causal, Bc):
+    inp = synth.make_inputs(1, 2, 2, 53, 8, dtype, sharp=True, seed=21)
+    scale = 0.7
+    o, lse = oracle.attn(inp.q, inp.k, inp.v, dtype=dtype, causal=causal, scale=scale, mode=oracle.EXACT_TILE,
+                         descale=(1.0, 1.0, 1.0), Bc=Bc)
+    c1 = np.float32(oracle.c1(scale))
+    off = 8 if dtype == FP8 else 0
+    vdec = (synth.bf16_decode(inp.v) if dtype == BF16 else synth.e4m3_decode(inp.v)).astype(np.float64)
+    for h in range(2):
+        for i in (0, 7, 26, 52):
+            s = oracle.logits_row(inp.q, inp.k, dtype, 0, h, i)
+            jend = i + 1 if causal else 53
+            o_ref, lse_ref = exact_tile_prefix_form(s, vdec[0, h], jend, c1, Bc, off, dtype)
+            # the only step not fixed to the bit is the fp64 exp2 before its
+            # fp32 rounding (libm's exp2 here, pow in the form above)
+            assert np.max(np.abs(o[0, h, i] - o_ref)) < 1e-9 * np.max(np.abs(vdec))
+            assert abs(lse[0, h, i] - lse_ref) < 1e-9
+
+
+@pytest.mark.parametrize("k,mode", [(1, oracle.H15_TILE), (2, oracle.SQ4_TILE), (3, oracle.SQ8_TILE)])
+@pytest.mark.parametrize("causal", [False, True])
+def test_row_exponents_reproduce_the_weights(k, mode, causal):
+    # y[j] = fp32(s_j ck + fp32(-M_t ck + 2^k off)) with M_t the prefix max of
+    # key j's tile (anchor[j]); the weight realisation applied to y gives W.
+    inp = synth.make_inputs(1, 1, 1, 90, 16, FP8, sharp=True, seed=22)
+    sc = 0.2
+    c1 = np.float32(oracle.c1(sc, inp.descale[0], inp.descale[1]))
+    Bc = 32
+    for i in (5, 40, 89):
+        s = oracle.logits_row(inp.q, inp.k, FP8, 0, 0, i)
+        y, anchor, w = oracle.row_exponents_from_logits(s, i, causal, float(c1), FP8, Bc, k=k)
+        w2, _, _ = oracle.sq_row_from_logits(s, i, causal, float(c1), FP8, Bc, k=k)
+        assert np.array_equal(w.view(np.uint32), w2.view(np.uint32))
+        jend = i + 1 if causal else 90
+        assert np.all(np.isneginf(y[jend:])) and np.all(np.isneginf(anchor[jend:]))
+        ck = Fraction(float(c1)) * 2 ** k
+        m = -np.inf
+        for j in range(jend):
+            if j % Bc == 0:
+                m = max(m, float(np.max(s[j:min(j + Bc, jend)])))
+            assert anchor[j] == np.float32(m)
+            nb = round_f32(-Fraction(m) * ck + 2 ** k * 8)
+            assert y[j] == round_f32(Fraction(float(s[j])) * ck + Fraction(float(nb)))
+            assert w[j] == np.float32(oracle.sq_weight(float(y[j]), k))
