@@ -1,21 +1,15 @@
 """GPU parity: the HIP kernels (through the C ABI) against the CPU oracle.
 
-Tolerances: max |O_gpu - O_oracle| <= 2e-2 max|V| for BF16 operands and
-6e-2 max|V| for FP8, with V the dequantised values.  EXACT mode is compared
-with the oracle's exact softmax on its own (fp64) logits, H15 with the
-oracle's per-tile Rowmax-H15 on its own fp32 logits.  LSE: 1e-3 for EXACT;
-for H15 against the oracle's own logits the median row must agree to 1e-4
-and every row to 5e-2 (a weight on the other side of an RNE boundary, caused
-by the fp32 accumulation order of the logit, moves LSE by a fraction of that
-weight), and against the oracle fed the GPU's own logits to 1e-5 plus the
-fp32 summation bound of l, (tiles + 64) 2^-24 (it passes 1e-5 beyond about
-13K keys); each LSE bar also allows four fp32 ulps of |LSE| (the
-stored value's own rounding, which exceeds 1e-5 once |LSE| is in the
-thousands).  The H15
-weights and stored P are compared bit for bit when the oracle is fed the
-GPU's own fp32 logits.  The finer input-rounding weights S(Q_{2^-k}) for
-k = 2, 3 (exp modes SQ4, SQ8) are held to the same bars as H15, and so is
-Rowmax-PoT (BF16) against the fp64 operator of Eq. (rowmax-pot), with its W
+Bars (parity_helpers): max |O_gpu - O_oracle| <= 2e-2 max|V| for BF16
+operands and 6e-2 max|V| for FP8, with V the dequantised values.  EXACT mode
+is compared with the oracle's exact softmax on its own (fp64) logits, the
+lattice weights (H15, S(Q_{1/4}), S(Q_{1/8})) with the oracle's per-tile
+recurrence on its own fp32 logits.  LSE: 1e-3 for EXACT; for the lattice
+weights each row within the bound that the GPU's logit accuracy implies
+(lse_bound_lattice) and the median row within 1e-4; against the oracle fed
+the GPU's own logits to 1e-5 plus the fp32 summation bound of l, with the
+weights and stored P bit for bit.  Rowmax-PoT (BF16) is held to the fp64
+operator of Eq. (rowmax-pot) (LSE: median 1e-4, every row 5e-2), with its W
 and P bit-exact against the row form of the oracle fed the GPU's logits."""
 import math
 import sys
@@ -27,76 +21,10 @@ import torch
 import oracle
 import paper_2609_33586_amd as pkg
 from paper_2609_33586_amd import synth
+from parity_helpers import (ALL_MODES, APPROX, BF16, EXACT, FP8, H15, ORDER, POT, SQ4, SQ8, TOL, assert_close,
+                            check_probe, dev_tensors, gpu_run, oracle_run, say, scale_of, stratified_rows, vmax)
 
 pytestmark = pytest.mark.gpu
-
-BF16, FP8 = synth.BF16, synth.FP8_E4M3
-EXACT, H15, SQ4, SQ8 = pkg.ATTN_EXP_EXACT, pkg.ATTN_EXP_H15, pkg.ATTN_EXP_SQ4, pkg.ATTN_EXP_SQ8
-APPROX = (H15, SQ4, SQ8)
-ALL_MODES = (EXACT,) + APPROX
-POT = pkg.ATTN_EXP_ROWMAX_POT  # BF16 only
-ORACLE_MODE = {EXACT: oracle.EXACT, H15: oracle.H15_TILE, SQ4: oracle.SQ4_TILE, SQ8: oracle.SQ8_TILE,
-               POT: oracle.ROWMAX_POT}
-ORDER = {H15: 1, SQ4: 2, SQ8: 3}  # input-rounding exponent k
-TOL = {BF16: 2e-2, FP8: 6e-2}
-LSE_TOL = 1e-3
-LSE_TOL_H15 = 5e-2
-
-
-def say(msg):
-    print(msg, flush=True)
-    sys.stdout.flush()
-
-
-def dev_tensors(inp):
-    d = torch.device("cuda:0")
-    if inp.dtype == BF16:
-        return tuple(torch.from_numpy(x.view(np.int16)).to(d).view(torch.bfloat16) for x in (inp.q, inp.k, inp.v))
-    return tuple(torch.from_numpy(x).to(d).view(torch.float8_e4m3fn) for x in (inp.q, inp.k, inp.v))
-
-
-def vmax(inp):
-    dec = synth.bf16_decode(inp.v) if inp.dtype == BF16 else synth.e4m3_decode(inp.v) * inp.descale[2]
-    return float(np.max(np.abs(dec)))
-
-
-def scale_of(d):
-    return float(np.float32(1.0 / math.sqrt(d)))
-
-
-def gpu_run(inp, causal, scale, mode, tensors=None):
-    q, k, v = tensors if tensors is not None else dev_tensors(inp)
-    o, lse = pkg.attn_fwd_ex(q, k, v, causal=causal, scale=scale, exp_mode=mode, descale=inp.descale)
-    torch.cuda.synchronize()
-    return o.float().cpu().numpy().astype(np.float64), lse.cpu().numpy().astype(np.float64)
-
-
-def oracle_run(inp, causal, scale, mode, rows=None):
-    om = ORACLE_MODE[mode]
-    return oracle.attn(inp.q, inp.k, inp.v, dtype=inp.dtype, causal=causal, scale=scale, mode=om,
-                       descale=inp.descale, Bc=pkg.attn_tile_bc(), rows=rows)
-
-
-def assert_close(inp, o, lse, o_ref, lse_ref, what, mode=EXACT):
-    err = float(np.max(np.abs(o - o_ref)))
-    # LSE is stored in fp32: at large logits (|LSE| in the thousands) its own
-    # rounding, a few ulps, is part of every bar below
-    dl = np.maximum(np.abs(lse - lse_ref) - 4.0 * np.spacing(np.abs(lse_ref).astype(np.float32)), 0.0)
-    lerr = float(np.max(dl))
-    bound = TOL[inp.dtype] * vmax(inp)
-    say(f"  {what}: max|dO| {err:.3e} (bound {bound:.3e})  max|dLSE| {lerr:.3e}  "
-        f"rows |dLSE|>1e-4: {np.mean(dl > 1e-4):.4f}")
-    assert np.all(np.isfinite(o)) and np.all(np.isfinite(lse))
-    assert err <= bound, what
-    if mode in APPROX or mode == POT:
-        # Against the oracle's own logits, a few weights sit on the other side
-        # of an RNE boundary (fp32 accumulation order of the logits), which
-        # moves LSE by a fraction of one weight; the exact LSE check is the
-        # one fed with the GPU's logits (test_probe_weights_bit_exact).
-        assert float(np.median(dl)) <= 1e-4 and lerr <= LSE_TOL_H15, what
-    else:
-        assert lerr <= LSE_TOL, what
-
 
 SMALL = [(dt, d, causal, S) for dt in (BF16, FP8) for d in (64, 128) for causal in (False, True)
          for S in (256, 300)]
@@ -110,69 +38,7 @@ def test_small_full_parity(dt, d, causal, S, mode):
     say(f"small dtype={dt} d={d} causal={causal} S={S} mode={mode}")
     o, lse = gpu_run(inp, causal, sc, mode)
     o_ref, lse_ref = oracle_run(inp, causal, sc, mode)
-    assert_close(inp, o, lse, o_ref.reshape(o.shape), lse_ref.reshape(lse.shape), "full", mode)
-
-
-def check_probe(inp, S, d, dt, causal, mode, sc, rowsets):
-    """Probe rows of the kernel: logits close to the exact dot products, and W,
-    P and LSE bit-identical (to 1e-5 for LSE) to the oracle fed those logits."""
-    q, k, v = dev_tensors(inp)
-    c1 = oracle.c1(sc, inp.descale[0], inp.descale[1])
-    G = inp.q.shape[1] // inp.k.shape[1]
-    for (b, h, r0, n) in rowsets:
-        say(f"probe dtype={dt} causal={causal} mode={mode} rows {r0}+{n} head {h}")
-        o_p, lse_p, s, w, pbits = pkg.attn_fwd_probe(q, k, v, causal=causal, scale=sc, exp_mode=mode,
-                                                     b=b, h=h, row0=r0, nrows=n, descale=inp.descale)
-        o_m, lse_m = pkg.attn_fwd_ex(q, k, v, causal=causal, scale=sc, exp_mode=mode, descale=inp.descale)
-        torch.cuda.synchronize()
-        # the probe runs the same arithmetic as the timed kernel
-        assert torch.equal(o_p.view(torch.int16), o_m.view(torch.int16))
-        assert torch.equal(lse_p, lse_m)
-        s, w, pbits = s.cpu().numpy(), w.cpu().numpy(), pbits.cpu().numpy().astype(np.uint32)
-        lse_p = lse_p.cpu().numpy()
-        dec = synth.bf16_decode if dt == BF16 else synth.e4m3_decode
-        qv = np.asarray(dec(inp.q[b, h]), np.float64)
-        kv = np.asarray(dec(inp.k[b, h // G]), np.float64)
-        for r in range(n):
-            i = r0 + r
-            jend = i + 1 if causal else S
-            # GPU logits agree with the exact dot products to within the MFMA's
-            # accumulation error, measured relative to sum_c |q_c k_c|: 2^-16
-            # for bf16 (fp32 accumulation); the fp8 MFMA sums its 64 products
-            # less exactly, so fp8 is held to 2^-12.
-            s_ref = oracle.logits_row(inp.q, inp.k, dt, b, h, i)
-            mag = np.abs(kv[:jend]) @ np.abs(qv[i])
-            assert np.all(np.isneginf(s[r, jend:]))
-            rel = np.max(np.abs(s[r, :jend] - s_ref[:jend]) / np.maximum(mag, 1e-30))
-            if r == 0:
-                say(f"  logit error / sum|q k|: {rel:.3e}")
-            assert rel <= (2.0 ** -16 if dt == BF16 else 2.0 ** -12)
-            if mode in APPROX:
-                w_ref, p_ref, lse_ref = oracle.sq_row_from_logits(s[r], i, causal, c1, dt, pkg.attn_tile_bc(),
-                                                                  k=ORDER[mode])
-            else:
-                w_ref, p_ref, lse_ref = oracle.h15_row_from_logits(s[r], i, causal, c1, dt, pkg.attn_tile_bc(),
-                                                                   exact_exp=True)
-            if mode in APPROX:
-                # LSE is an fp32 value formed from m c1 + log2 l: at large
-                # logits (|LSE| in the thousands) a few of its ulps exceed 1e-5.
-                # l itself is an fp32 sum of positive weights, one add per key
-                # tile into the running sum after in-tile partial sums, so its
-                # relative error is bounded by (tiles + 64) 2^-24; that bound
-                # passes 1e-5 beyond about 104 tiles (13K keys).
-                sum_bound = (jend / pkg.attn_tile_bc() + 64) * 2.0 ** -24
-                lse_tol = max(1e-5, 4.0 * float(np.spacing(np.float32(abs(lse_ref))))) + sum_bound
-                assert abs(lse_p[b, h, i] - lse_ref) <= lse_tol, f"row {i}"
-                assert np.array_equal(w[r].view(np.uint32), w_ref.view(np.uint32)), f"row {i}"
-                assert np.array_equal(pbits[r], p_ref), f"row {i}"
-            else:
-                # hardware exp2 (about 1 ulp); P is the stored rounding of the GPU's own w
-                assert np.max(np.abs(w[r] - w_ref) / np.maximum(w_ref, 1e-30)) < 4e-7
-                _, p_own, _ = oracle.h15_row_from_logits(s[r], i, causal, c1, dt, pkg.attn_tile_bc(), exact_exp=True)
-                enc = np.array([(int(np.array([x], np.float32).view(np.uint32)[0]) + 0x7FFF +
-                                 ((int(np.array([x], np.float32).view(np.uint32)[0]) >> 16) & 1)) >> 16
-                                if dt == BF16 else oracle.e4m3_encode(float(x)) for x in w[r]], np.uint32)
-                assert np.array_equal(pbits[r], enc), f"row {i}"
+    assert_close(inp, o, lse, o_ref, lse_ref, "full", mode, causal=causal, sc=sc)
 
 
 @pytest.mark.parametrize("dt", [BF16, FP8])
@@ -280,7 +146,7 @@ def test_fp8_saturated_logits_at_the_narrow_clamp_limit(side, mode):
     check_probe(inp, S, d, FP8, True, mode, sc, ((0, 0, 0, 40), (0, 0, S - 40, 40)))
     o, lse = gpu_run(inp, True, sc, mode)
     o_ref, lse_ref = oracle_run(inp, True, sc, mode)
-    assert_close(inp, o, lse, o_ref, lse_ref, f"saturated logits, bound {bound:.0f}", mode)
+    assert_close(inp, o, lse, o_ref, lse_ref, f"saturated logits, bound {bound:.0f}", mode, causal=True, sc=sc)
 
 
 @pytest.mark.parametrize("causal", [False, True])
@@ -298,7 +164,7 @@ def test_fp8_unit_descales_float_clamp_path(causal, mode):
     check_probe(inp, S, d, FP8, causal, mode, sc, ((0, 0, 0, 30), (0, 1, S - 30, 30)))
     o, lse = gpu_run(inp, causal, sc, mode)
     o_ref, lse_ref = oracle_run(inp, causal, sc, mode)
-    assert_close(inp, o, lse, o_ref, lse_ref, "unit descales", mode)
+    assert_close(inp, o, lse, o_ref, lse_ref, "unit descales", mode, causal=causal, sc=sc)
 
 
 @pytest.mark.parametrize("dt", [BF16, FP8])
@@ -319,7 +185,7 @@ def test_one_hot_value_gates(dt, S):
         say(f"one-hot gate dtype={dt} S={S} block {blk}")
         o, lse = gpu_run(inp, True, sc, H15)
         o_ref, lse_ref = oracle_run(inp, True, sc, H15)
-        assert_close(inp, o, lse, o_ref, lse_ref, "one-hot", H15)
+        assert_close(inp, o, lse, o_ref, lse_ref, "one-hot", H15, causal=True, sc=sc)
         # read back probabilities and check the normalized octave bound against
         # exact softmax (App. B.2: +-0.585 plus storage rounding allowances)
         p_gpu = o[0, :, :, :]
@@ -350,13 +216,11 @@ def test_full_size_sampled_rows(w, mode):
     assert np.all(np.isfinite(o)) and np.all(np.isfinite(lse))
     # O is a convex combination of V rows (times the descale)
     assert np.max(np.abs(o)) <= vmax(inp) * (1 + 2 ** -7)
-    rng = np.random.default_rng(7)
-    nrows_total = w.B * w.Hq * w.S
-    fixed = [0, w.S - 1, w.S // 2, 255, 256, nrows_total - 1, nrows_total - w.S]
-    rows = np.unique(np.concatenate([fixed, rng.integers(0, nrows_total, 17)]))
+    rows = stratified_rows(w.B, w.Hq, w.S, 256 if w.dtype == BF16 else 128, seed=7)
     say(f"full-size {w.name} mode={mode}: oracle on {len(rows)} rows")
     o_ref, lse_ref = oracle_run(inp, w.causal, sc, mode, rows=rows)
-    assert_close(inp, o.reshape(-1, w.d)[rows], lse.reshape(-1)[rows], o_ref, lse_ref, "sampled rows", mode)
+    assert_close(inp, o.reshape(-1, w.d)[rows], lse.reshape(-1)[rows], o_ref, lse_ref, "sampled rows", mode,
+                 causal=w.causal, sc=sc, rows=rows)
 
 
 @pytest.mark.parametrize("dt,S,causal", [(FP8, 1 << 20, False), (BF16, 1 << 19, True)])
@@ -377,7 +241,8 @@ def test_long_sequence_offsets(dt, S, causal):
     rows = np.array([0, 127, 128, S // 2 - 1, S // 2, S - 129, S - 128, S - 1])
     say(f"long sequence dt={dt} S={S}: oracle on {len(rows)} rows")
     o_ref, lse_ref = oracle_run(inp, causal, sc, H15, rows=rows)
-    assert_close(inp, o.reshape(-1, d)[rows], lse.reshape(-1)[rows], o_ref, lse_ref, "long sequence rows", H15)
+    assert_close(inp, o.reshape(-1, d)[rows], lse.reshape(-1)[rows], o_ref, lse_ref, "long sequence rows", H15,
+                 causal=causal, sc=sc, rows=rows)
     check_probe(inp, S, d, dt, causal, H15, sc, ((0, 0, S - 3, 3),))
 
 
@@ -436,7 +301,8 @@ def test_xcd_grouped_orders_write_every_row(dt):
         assert not torch.isnan(o.float()).any() and not torch.isnan(lse).any()
         o_ref, lse_ref = oracle_run(inp, causal, sc, H15, rows=rows)
         assert_close(inp, o.float().cpu().numpy().astype(np.float64).reshape(-1, 128)[rows],
-                     lse.cpu().numpy().astype(np.float64).reshape(-1)[rows], o_ref, lse_ref, "grouped order", H15)
+                     lse.cpu().numpy().astype(np.float64).reshape(-1)[rows], o_ref, lse_ref, "grouped order", H15,
+                     causal=causal, sc=sc, rows=rows)
 
 
 EDGE = [(1, 1, 1, 1, 64), (1, 1, 1, 2, 128), (1, 2, 1, 31, 128), (2, 3, 3, 129, 64), (1, 8, 1, 255, 128),
@@ -453,7 +319,7 @@ def test_edge_shapes(B, Hq, Hkv, S, d, dt):
             say(f"edge B={B} Hq={Hq} Hkv={Hkv} S={S} d={d} dtype={dt} causal={causal} mode={mode}")
             o, lse = gpu_run(inp, causal, sc, mode)
             o_ref, lse_ref = oracle_run(inp, causal, sc, mode)
-            assert_close(inp, o, lse, o_ref, lse_ref, "edge", mode)
+            assert_close(inp, o, lse, o_ref, lse_ref, "edge", mode, causal=causal, sc=sc)
 
 
 def test_side_stream_and_lse_optional():
@@ -478,7 +344,7 @@ def test_rowmax_pot_small_full_parity(d, causal, S):
     say(f"rowmax-pot d={d} causal={causal} S={S}")
     o, lse = gpu_run(inp, causal, sc, POT)
     o_ref, lse_ref = oracle_run(inp, causal, sc, POT)
-    assert_close(inp, o, lse, o_ref.reshape(o.shape), lse_ref.reshape(lse.shape), "rowmax-pot", POT)
+    assert_close(inp, o, lse, o_ref, lse_ref, "rowmax-pot", POT)
 
 
 def check_pot_probe(inp, S, causal, sc, rowsets):
@@ -527,3 +393,20 @@ def test_rowmax_pot_full_size(w):
     o_ref, lse_ref = oracle_run(inp, w.causal, sc, POT, rows=rows)
     assert_close(inp, o.reshape(-1, w.d)[rows], lse.reshape(-1)[rows], o_ref, lse_ref, "rowmax-pot sampled", POT)
     check_pot_probe(inp, w.S, w.causal, sc, ((w.B - 1, w.Hq - 1, w.S - 40, 40),))
+
+
+@pytest.mark.parametrize("mode", [EXACT, H15])
+def test_attn_fwd_fp8_takes_unit_descales(mode):
+    # attn_fwd has no descale arguments: FP8 operands are taken as stored,
+    # the same as attn_fwd_ex with descales (1, 1, 1)
+    inp = synth.make_inputs(1, 4, 2, 300, 128, FP8, sharp=True, seed=990)
+    q, k, v = dev_tensors(inp)
+    sc = scale_of(128)
+    o1, l1 = pkg.attn_fwd(q, k, v, causal=True, scale=sc, exp_mode=mode)
+    o2, l2 = pkg.attn_fwd_ex(q, k, v, causal=True, scale=sc, exp_mode=mode, descale=(1.0, 1.0, 1.0))
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16)) and torch.equal(l1, l2)
+    unit = synth.Inputs(inp.q, inp.k, inp.v, (1.0, 1.0, 1.0), FP8)
+    o_ref, lse_ref = oracle_run(unit, True, sc, mode)
+    assert_close(unit, o1.float().cpu().numpy().astype(np.float64), l1.cpu().numpy().astype(np.float64), o_ref,
+                 lse_ref, "attn_fwd fp8", mode, causal=True, sc=sc)
