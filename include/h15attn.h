@@ -67,6 +67,7 @@
 #ifndef H15ATTN_H
 #define H15ATTN_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -142,6 +143,76 @@ int attn_fwd_probe(const void* q, const void* k, const void* v, void* o, float* 
                    int Hkv, int S, int d, int causal, float scale, int dtype, int exp_mode,
                    const attn_opts* opts, int b, int h, int row0, int nrows, float* s_out,
                    float* w_out, uint32_t* p_bits_out);
+
+/* ---- Decode over a key/value cache -------------------------------------
+ *
+ * Sq query rows per query head attend to the first Sk rows of a key/value
+ * cache (App. A.1's attention with the queries of the last Sq positions; the
+ * paper leaves decode outside its scope, this is the library's extension).
+ * Query position i (0 <= i < Sq) sees keys j <= Sk - Sq + i when causal
+ * (bottom-right alignment: the last query row sees the whole cache; with
+ * Sq = Sk it is attn_fwd's causal mask), every key otherwise.
+ *
+ * Key parts: the keys are cut into consecutive parts of split_keys keys (a
+ * multiple of attn_tile_bc(); 0, or any value >= Sk, gives one part), which
+ * run in parallel.  Within a part the weights follow the recurrence described
+ * above for attn_fwd, over the part's keys only: its tiles start at the
+ * part's first key and its running maximum starts afresh, so for the lattice
+ * weights (ATTN_EXP_H15, SQ4, SQ8) the cut is part of the result (each
+ * weight is rounded relative to its own part's running maximum).  The parts
+ * then merge exactly:
+ *     m = max_p m_p,   f_p = 2^(c1 (m_p - m)),   l = sum_p f_p l_p,
+ *     O = (sum_p f_p O_p) / l * v_descale,   LSE = ln2 (m c1 + log2 l - off),
+ * with m_p, l_p, O_p a part's final running maximum, row sum and unnormalised
+ * output (parts holding no visible key of a row take no part in its merge).
+ * With one part the result equals attn_fwd's rows of the same keys.  The
+ * exact control does not depend on the cut beyond rounding.  For a given
+ * split_keys the result is deterministic; attn_decode_split_keys() proposes
+ * one that fills the GPU and is a function of the shape only.
+ *
+ * Layouts: q: [B][Hq][Sq][d]; k, v: [B][Hkv][Sk_cap][d], the first Sk rows of
+ * each head being the cache (rows Sk .. Sk_cap - 1 are never read); o:
+ * [B][Hq][Sq][d] bf16; lse: [B][Hq][Sq] fp32 (may be NULL).  Element types,
+ * GQA mapping, descales, stream and exp_mode as for attn_fwd_ex; the rescale
+ * threshold must be 0 and Rowmax-PoT is not offered (ATTN_EUNSUPPORTED).
+ *
+ * Workspace: with more than one part the library keeps each part's (m, l, O)
+ * in a caller-provided device buffer of at least
+ * attn_decode_workspace_bytes() bytes, 16-byte aligned (else ATTN_EINVAL);
+ * with one part it may be NULL.  Nothing in it needs initialising; two calls
+ * in flight at once must not share it.  The call launches two kernels on the
+ * stream (the parts, then their merge), one when there is a single part.
+ *
+ * Errors (besides those of attn_fwd_ex): ATTN_EINVAL for Sq > Sk,
+ * Sk > Sk_cap, split_keys negative or not a multiple of attn_tile_bc(), or a
+ * missing or short workspace; ATTN_EUNSUPPORTED for one head's cache of
+ * Sk_cap * d * element bytes beyond 2^31 - 1, B * Hq * Sq > 2^30, or a
+ * nonzero rescale threshold. */
+int attn_decode(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq, int Hkv,
+                int Sq, int Sk, int Sk_cap, int d, int causal, float scale, int dtype, int exp_mode,
+                int split_keys, void* workspace, size_t workspace_bytes, const attn_opts* opts);
+
+/* Bytes of workspace attn_decode needs for this shape and cut (0 for one
+ * part, or for invalid sizes). */
+size_t attn_decode_workspace_bytes(int B, int Hq, int Sq, int Sk, int d, int split_keys);
+
+/* A cut (split_keys) for attn_decode that gives about two workgroups per
+ * compute unit with at least four key tiles per part, or 0 (one part) when
+ * the shape fills the GPU without cutting.  A function of its arguments
+ * only; 0 for invalid sizes. */
+int attn_decode_split_keys(int B, int Hq, int Hkv, int Sq, int Sk, int d, int dtype);
+
+/* Test access to decode's intermediate values, as attn_fwd_probe: runs the
+ * same kernels as attn_decode (O and LSE written identically) and stores, for
+ * query row (b, h, i), the fp32 raw logits s, the fp32 weights w (relative
+ * to the running maximum of the key's tile within its part) and the P bits
+ * of every cache key: s_out, w_out, p_bits_out are device buffers of Sk
+ * elements.  Keys the row does not see are written as s = -inf, w = 0,
+ * P = 0.  Requires 0 <= b < B, 0 <= h < Hq, 0 <= i < Sq (else ATTN_EINVAL). */
+int attn_decode_probe(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq, int Hkv,
+                      int Sq, int Sk, int Sk_cap, int d, int causal, float scale, int dtype, int exp_mode,
+                      int split_keys, void* workspace, size_t workspace_bytes, const attn_opts* opts, int b,
+                      int h, int i, float* s_out, float* w_out, uint32_t* p_bits_out);
 
 /* Static description of an error code. */
 const char* attn_strerror(int code);

@@ -21,7 +21,8 @@ ATTN_EXP_EXACT, ATTN_EXP_H15, ATTN_EXP_SQ4, ATTN_EXP_SQ8, ATTN_EXP_ROWMAX_POT = 
 ATTN_OK, ATTN_EINVAL, ATTN_EUNSUPPORTED, ATTN_ELAUNCH = 0, -1, -2, -3
 
 # every symbol the header declares
-EXPORTS = ("attn_fwd", "attn_fwd_ex", "attn_fwd_probe", "attn_strerror", "attn_tile_bc")
+EXPORTS = ("attn_fwd", "attn_fwd_ex", "attn_fwd_probe", "attn_strerror", "attn_tile_bc", "attn_decode",
+           "attn_decode_workspace_bytes", "attn_decode_split_keys", "attn_decode_probe")
 
 
 class attn_opts(ctypes.Structure):
@@ -59,6 +60,15 @@ def lib() -> ctypes.CDLL:
     L.attn_strerror.restype = ctypes.c_char_p
     L.attn_tile_bc.argtypes = []
     L.attn_tile_bc.restype = I
+    dec = [P, P, P, P, P, I, I, I, I, I, I, I, I, F, I, I, I, P, ctypes.c_size_t, ctypes.POINTER(attn_opts)]
+    L.attn_decode.argtypes = dec
+    L.attn_decode.restype = I
+    L.attn_decode_probe.argtypes = dec + [I, I, I, P, P, P]
+    L.attn_decode_probe.restype = I
+    L.attn_decode_workspace_bytes.argtypes = [I, I, I, I, I, I]
+    L.attn_decode_workspace_bytes.restype = ctypes.c_size_t
+    L.attn_decode_split_keys.argtypes = [I, I, I, I, I, I, I]
+    L.attn_decode_split_keys.restype = I
     _lib = L
     return L
 
@@ -157,4 +167,80 @@ def attn_fwd_probe(q, k, v, *, causal: bool, scale: float, exp_mode: int, b: int
                               s.data_ptr(), w.data_ptr(), pb.data_ptr())
     if rc != ATTN_OK:
         raise AttnError(rc, "attn_fwd_probe")
+    return out, lse, s, w, pb
+
+
+# ---- decode over a key/value cache ------------------------------------------
+
+def attn_decode_split_keys(B: int, Hq: int, Hkv: int, Sq: int, Sk: int, d: int, dtype: int) -> int:
+    """The library's proposed key cut for attn_decode (0: one part)."""
+    return int(lib().attn_decode_split_keys(int(B), int(Hq), int(Hkv), int(Sq), int(Sk), int(d), int(dtype)))
+
+
+def attn_decode_workspace_bytes(B: int, Hq: int, Sq: int, Sk: int, d: int, split_keys: int) -> int:
+    return int(lib().attn_decode_workspace_bytes(int(B), int(Hq), int(Sq), int(Sk), int(d), int(split_keys)))
+
+
+def _check_decode(q, k, v, Sk):
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if not t.is_cuda or not t.is_contiguous() or t.dim() != 4:
+            raise ValueError(f"{name} must be a contiguous 4-D device tensor")
+    B, Hq, Sq, d = q.shape
+    Hkv, cap = k.shape[1], k.shape[2]
+    if tuple(k.shape) != (B, Hkv, cap, d) or tuple(v.shape) != tuple(k.shape):
+        raise ValueError("k and v must be [B,Hkv,Sk_cap,d] with q's B and d")
+    dt = _dtype_of(q)
+    if _dtype_of(k) != dt or _dtype_of(v) != dt:
+        raise TypeError("q, k, v must share one operand type")
+    return B, Hq, Hkv, Sq, (cap if Sk is None else int(Sk)), cap, d, dt
+
+
+def _workspace(q, B, Hq, Sq, Sk, d, split_keys, workspace):
+    import torch
+    need = attn_decode_workspace_bytes(B, Hq, Sq, Sk, d, split_keys)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device) if need else None
+    ptr = workspace.data_ptr() if workspace is not None else None
+    nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    return workspace, ptr, nbytes
+
+
+def attn_decode(q, k, v, *, causal: bool, scale: float, exp_mode: int, split_keys: int, Sk: int | None = None,
+                descale=None, stream=None, out=None, lse=None, want_lse: bool = True, workspace=None):
+    """Decode over a key/value cache (see include/h15attn.h, attn_decode).
+
+    q: [B,Hq,Sq,d]; k, v: [B,Hkv,Sk_cap,d] whose first Sk rows (default all)
+    are the cache.  Returns (O [B,Hq,Sq,d] bf16, LSE [B,Hq,Sq] fp32 or None).
+    workspace: a device buffer of attn_decode_workspace_bytes() bytes
+    (allocated here when None and the cut has several parts)."""
+    B, Hq, Hkv, Sq, Sk, cap, d, dt = _check_decode(q, k, v, Sk)
+    out, lse = _outputs(q, out, lse, want_lse)
+    ws, wptr, wbytes = _workspace(q, B, Hq, Sq, Sk, d, split_keys, workspace)
+    opts = _opts(descale, stream)
+    rc = lib().attn_decode(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                           lse.data_ptr() if lse is not None else None, B, Hq, Hkv, Sq, Sk, cap, d,
+                           int(bool(causal)), float(scale), dt, int(exp_mode), int(split_keys), wptr, wbytes,
+                           ctypes.byref(opts))
+    if rc != ATTN_OK:
+        raise AttnError(rc, "attn_decode")
+    return out, lse
+
+
+def attn_decode_probe(q, k, v, *, causal: bool, scale: float, exp_mode: int, split_keys: int, b: int, h: int,
+                      i: int, Sk: int | None = None, descale=None, stream=None):
+    """Returns (O, LSE, s, w, p_bits) with s/w/p_bits of shape [Sk] for query row (b, h, i)."""
+    import torch
+    B, Hq, Hkv, Sq, Sk, cap, d, dt = _check_decode(q, k, v, Sk)
+    out, lse = _outputs(q, None, None, True)
+    ws, wptr, wbytes = _workspace(q, B, Hq, Sq, Sk, d, split_keys, None)
+    s = torch.empty(Sk, dtype=torch.float32, device=q.device)
+    w = torch.empty(Sk, dtype=torch.float32, device=q.device)
+    pb = torch.empty(Sk, dtype=torch.int32, device=q.device)
+    opts = _opts(descale, stream)
+    rc = lib().attn_decode_probe(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr(), B, Hq,
+                                 Hkv, Sq, Sk, cap, d, int(bool(causal)), float(scale), dt, int(exp_mode),
+                                 int(split_keys), wptr, wbytes, ctypes.byref(opts), int(b), int(h), int(i),
+                                 s.data_ptr(), w.data_ptr(), pb.data_ptr())
+    if rc != ATTN_OK:
+        raise AttnError(rc, "attn_decode_probe")
     return out, lse, s, w, pb

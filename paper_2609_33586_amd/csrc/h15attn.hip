@@ -36,6 +36,8 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef int i32x8 __attribute__((ext_vector_type(8)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x2v __attribute__((__vector_size__(2 * sizeof(int))));
@@ -1031,6 +1033,545 @@ hipError_t launch_any(const Params& p, int dtype, int d, int causal, int mode, h
                   : launch_dt_d<DT_FP8, 64, PROBE>(p, causal, mode, st);
 }
 
+// ---------------------------------------------------------------------------
+// Decode over a key/value cache: Sq query rows per head against Sk cached
+// keys (bottom-right causal alignment), the keys cut into parts of
+// split_keys keys that workgroups take in parallel.  Within a part the
+// per-tile recurrence runs as in the forward kernel, with tiles starting at
+// the part's first key and the running maximum starting at -inf; the parts'
+// (m, l, O) then merge exactly (attn_decode_merge).  One part: the kernel
+// normalises and writes O and LSE itself.
+//
+// One workgroup = 4 waves for one (batch, KV head, block of 32 query rows,
+// part).  The 32 rows are the G * Sq query rows of the KV head's query heads
+// (row r: head h = hkv G + r / Sq, position r % Sq), so the K/V tiles are read
+// once for all of them.  Wave w computes the scores of keys 32w .. 32w + 31
+// of each 128-key tile (one 32x32 block of S^T = K Q^T) and their share of
+// PV; the tile maximum of each row is combined across the four waves through
+// LDS, so every wave moves the same running maximum at every tile, and the
+// waves' partial row sums and O accumulators, all relative to that maximum,
+// are added up at the end.
+
+struct DecParams {
+  const uint8_t* q;
+  const uint8_t* k;
+  const uint8_t* v;
+  uint16_t* o;
+  float* lse;
+  float* part_o;   // [rows][nsplit][d], unnormalised O of each part (nsplit > 1)
+  float* part_ml;  // [rows][nsplit][2], (m, l) of each part (nsplit > 1)
+  int B, Hq, Hkv, Sq, Sk, Sk_cap, G, R, nrb, nsplit, split_keys;
+  float c1, ck, vd;
+  // probe target (PROBE instantiations only): output row (pb, ph, pi)
+  int pb, ph, pi;
+  float* s_out;
+  float* w_out;
+  uint32_t* p_out;
+};
+
+constexpr int DEC_NW = 4;  // waves per decode workgroup (one 32-key block each)
+
+__device__ __forceinline__ void settle_block(f32x16& v) {
+  // as settle_scores, for one block
+  asm("s_nop 15\n\ts_nop 7" : "+v"(v));
+}
+
+template <int E = 0>
+__device__ __forceinline__ void mask_beyond1(f32x16& v, int lim, float y) {
+  if constexpr (E < 16) {
+    v[E] = select_beyond<8 * (E >> 2) + (E & 3)>(lim, v[E], y);
+    mask_beyond1<E + 1>(v, lim, y);
+  }
+}
+
+__device__ __forceinline__ float block_max(const f32x16& v) {
+  // 16 -> 6 -> 2 -> 1
+  const float a0 = max3(v[0], v[1], v[2]), a1 = max3(v[3], v[4], v[5]), a2 = max3(v[6], v[7], v[8]);
+  const float a3 = max3(v[9], v[10], v[11]), a4 = max3(v[12], v[13], v[14]);
+  const float b0 = max3(a0, a1, a2), b1 = max3(a3, a4, v[15]);
+  return max3(b0, b1, b1);
+}
+
+template <int DT, int D, bool CAUSAL, int MODE, bool PROBE>
+__global__ __launch_bounds__(DEC_NW * 64) void attn_decode_kernel(DecParams p) {
+  using C = Cfg<DT, D>;
+  constexpr int NW = DEC_NW;
+  constexpr int NSTAGE = 2;
+  constexpr int NDB = D / 32;
+  constexpr int NKQ = DT == DT_BF16 ? D / 16 : D / 64;
+  constexpr int CHUNKS = C::CHUNKS;
+  static_assert(CHUNKS % (NW * 64) == 0, "tile/staging mismatch");
+  static_assert(NW * NDB * 16 * 64 * 4 <= NSTAGE * C::BUF, "the O reduction reuses the tile buffers");
+  __shared__ __attribute__((aligned(16))) uint8_t smem[NSTAGE * C::BUF];
+  __shared__ __attribute__((aligned(16))) float mx_lds[32][NW];
+  __shared__ float l_lds[NW][64];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int i32 = lane & 31;
+  const int g = lane >> 5;
+  const int G4 = lane >> 4, L16 = lane & 15;
+
+  int L = blockIdx.x;
+  const int split = L % p.nsplit;
+  L /= p.nsplit;
+  const int rb = L % p.nrb;
+  const int bkv = L / p.nrb;
+  const int b = bkv / p.Hkv, hkv = bkv - b * p.Hkv;
+  const int row = rb * WROWS + i32;
+  const bool row_ok = row < p.R;
+  const int rowc = min(row, p.R - 1);
+  const int gq = rowc / p.Sq, iq = rowc - gq * p.Sq;
+  const int h = hkv * p.G + gq;
+  const size_t orow = (size_t)(b * p.Hq + h) * (size_t)p.Sq + (size_t)iq;
+  const int Sk = p.Sk;
+  const int limit = CAUSAL ? Sk - p.Sq + iq : Sk - 1;  // last key this row sees
+  const int j0 = split * p.split_keys;
+  const int j1 = min(j0 + p.split_keys, Sk);
+  const int ntiles = (j1 - j0 + BC - 1) / BC;
+  const float off = DT == DT_FP8 ? 8.0f : 0.0f;
+
+  // ---- Q rows (MFMA B operand: lane holds row i32, k-half g)
+  const uint8_t* qptr = p.q + orow * C::RB;
+  bf16x8 qb16[DT == DT_BF16 ? NKQ : 1];
+  i32x8 qf8[DT == DT_FP8 ? NKQ : 1];
+  if constexpr (DT == DT_BF16) {
+#pragma unroll
+    for (int kk = 0; kk < NKQ; ++kk) qb16[kk] = *(const bf16x8*)(qptr + (16 * kk + 8 * g) * 2);
+  } else {
+#pragma unroll
+    for (int kk = 0; kk < NKQ; ++kk) qf8[kk] = *(const i32x8*)(qptr + 64 * kk + 32 * g);
+  }
+
+  // ---- staging of the part's tiles, as in the forward kernel; the buffer
+  // resource starts at the part's first key and ends at the cache length, so
+  // rows at or beyond Sk read as zero
+  const uint8_t* kg = p.k + ((size_t)bkv * (size_t)p.Sk_cap + (size_t)j0) * C::RB;
+  const uint8_t* vg = p.v + ((size_t)bkv * (size_t)p.Sk_cap + (size_t)j0) * C::RB;
+  const __amdgpu_buffer_rsrc_t krsrc =
+      __builtin_amdgcn_make_buffer_rsrc((void*)kg, (short)0, (Sk - j0) * C::RB, BUF_DWORD3);
+  const __amdgpu_buffer_rsrc_t vrsrc =
+      __builtin_amdgcn_make_buffer_rsrc((void*)vg, (short)0, (Sk - j0) * C::RB, BUF_DWORD3);
+  constexpr int WAVE_LOADS = CHUNKS / (NW * 64);
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  uint32_t koff_c[WAVE_LOADS], voff_c[WAVE_LOADS];
+#pragma unroll
+  for (int c = 0; c < WAVE_LOADS; ++c) {
+    const int slot = (c * NW + wave) * 64 + lane;
+    const int r = slot / C::NCH, pch = slot % C::NCH;
+    koff_c[c] = (uint32_t)(r * C::RB + ((pch ^ k_swz<DT, D>(r)) << 4));
+    voff_c[c] = (uint32_t)(r * C::RB + ((pch ^ v_swz<DT, D>(r)) << 4));
+  }
+  auto stage = [&](int t, uint8_t* dst, const __amdgpu_buffer_rsrc_t& rsrc,
+                   const uint32_t (&off_c)[WAVE_LOADS]) __attribute__((always_inline)) {
+    const uint32_t soff = (uint32_t)(t * BC) * C::RB;
+#pragma unroll
+    for (int c = 0; c < WAVE_LOADS; ++c) {
+      const uint32_t voff = off_c[c];
+      uint8_t* ldst = dst + (c * NW + wave_s) * 1024;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, LDS_PTR(void, ldst), 16, voff, soff, 0, 0);
+    }
+  };
+
+  // ---- V^T operand addresses (as the forward kernel's, moved to this
+  // wave's 32 keys; the swizzle repeats every 16 rows, so the move keeps it)
+  uint32_t vbase[NDB];
+  auto set_vbase = [&](const uint8_t* vl) __attribute__((always_inline)) {
+    const uint32_t vla = (uint32_t)(size_t)LDS_PTR(const uint8_t, vl) + (uint32_t)(32 * wave * C::RB);
+    if constexpr (DT == DT_BF16) {
+      const int vrow = 4 * (G4 >> 1) + (L16 >> 2);
+      const int vcolb = (16 * (G4 & 1) + 4 * (L16 & 3)) * 2;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const int cb = 64 * db + vcolb;
+        vbase[db] = vla + vrow * C::RB + (((cb >> 4) ^ v_swz<DT, D>(vrow)) << 4) + (cb & 15);
+      }
+    } else {
+      const int vrow = 4 * (G4 >> 1) + 8 * (L16 >> 3) + ((L16 >> 1) & 3);
+      const int vcol = 16 * (G4 & 1) + 8 * (L16 & 1);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        const int cb = 32 * db + vcol;
+        vbase[db] = vla + vrow * C::RB + (((cb >> 4) ^ v_swz<DT, D>(vrow)) << 4) + (cb & 15);
+      }
+    }
+  };
+
+  f32x16 oacc[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) oacc[db] = f32x16{0.0f};
+  float m_run = -INFINITY;
+  float l_part = 0.0f;
+  const bool probe_row = PROBE && row_ok && b == p.pb && h == p.ph && iq == p.pi;
+
+  stage(0, smem, krsrc, koff_c);
+  stage(0, smem + C::TILE, vrsrc, voff_c);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  for (int t = 0; t < ntiles; ++t) {
+    uint8_t* const kl = smem + (t & 1) * C::BUF;
+    uint8_t* const vl = kl + C::TILE;
+    if (t + 1 < ntiles) {
+      stage(t + 1, smem + ((t + 1) & 1) * C::BUF, krsrc, koff_c);
+      stage(t + 1, smem + ((t + 1) & 1) * C::BUF + C::TILE, vrsrc, voff_c);
+    }
+    const int kt0 = j0 + t * BC;    // first key of the tile
+    const int kw0 = kt0 + 32 * wave;  // first key of this wave's block
+
+    // ---- S^T block of this wave's 32 keys
+    f32x16 sv;
+    {
+      const uint8_t* rowp = kl + (32 * wave + i32) * C::RB;
+      const int kswz = k_swz<DT, D>(i32);  // == k_swz(32 wave + i32)
+      if constexpr (DT == DT_BF16) {
+        bf16x8 kop[NKQ];
+#pragma unroll
+        for (int kk = 0; kk < NKQ; ++kk) kop[kk] = *(const bf16x8*)(rowp + (((2 * kk + g) ^ kswz) << 4));
+#pragma unroll
+        for (int kk = 0; kk < NKQ; ++kk)
+          sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kk], qb16[kk], kk == 0 ? f32x16{0.0f} : sv, 0, 0, 0);
+      } else {
+        i32x8 kop[NKQ];
+#pragma unroll
+        for (int kk = 0; kk < NKQ; ++kk) {
+          const i32x4 lo = *(const i32x4*)(rowp + (((4 * kk + 2 * g) ^ kswz) << 4));
+          const i32x4 hi = *(const i32x4*)(rowp + (((4 * kk + 2 * g + 1) ^ kswz) << 4));
+          kop[kk] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        }
+#pragma unroll
+        for (int kk = 0; kk < NKQ; ++kk)
+          sv = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kop[kk], qf8[kk], kk == 0 ? f32x16{0.0f} : sv, 0, 0,
+                                                               0, 0, 0, 0);
+      }
+    }
+    settle_block(sv);
+
+    // ---- masking: keys beyond the row's limit or the cache
+    const bool need_mask = (CAUSAL && kt0 + BC - 1 > Sk - p.Sq) || (kt0 + BC > Sk);
+    const int lim = limit - kw0 - 4 * g;
+    if (need_mask) mask_beyond1(sv, lim, -INFINITY);
+    if constexpr (PROBE) {
+      if (probe_row) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int key = kw0 + 8 * (j >> 2) + 4 * g + (j & 3);
+          if (key < Sk) p.s_out[key] = sv[j];
+        }
+      }
+    }
+
+    // ---- the tile maximum of each row, over the four waves' blocks
+    {
+      float ma, mb;
+      with_partner(block_max(sv), ma, mb);
+      if (g == 0) mx_lds[i32][wave] = __builtin_fmaxf(ma, mb);
+    }
+    __syncthreads();
+    const f32x4 mx4 = *(const f32x4*)&mx_lds[i32][0];
+    const float m_new = max3(m_run, __builtin_fmaxf(mx4[0], mx4[1]), __builtin_fmaxf(mx4[2], mx4[3]));
+    // a row that has seen no key yet keeps m = -inf, l = 0, O = 0
+    const float alpha = m_new == -INFINITY ? 1.0f : __builtin_amdgcn_exp2f((m_run - m_new) * p.c1);
+    const float m_use = m_new == -INFINITY ? 0.0f : m_new;
+    m_run = m_new;
+
+    // ---- weights (in place), row sum, P
+    uint32_t wpk[8];
+    constexpr bool PACKED = mode_lattice(MODE);
+    if constexpr (PACKED) {
+      const float nbk = __builtin_fmaf(-m_use, p.ck, (float)(1 << mode_order(MODE)) * off);
+#pragma unroll
+      for (int j = 0; j < 16; ++j) sv[j] = __uint_as_float(sq_pre<MODE>(sv[j], p.ck, nbk));
+      if (need_mask) {
+        if constexpr (mode_narrow(MODE)) {
+          const float lift = __uint_as_float(0x4B3F0000u | sq_masked<MODE>());
+#pragma unroll
+          for (int j = 0; j < 16; ++j) sv[j] = max3(sv[j], lift, lift);
+        } else {
+          mask_beyond1(sv, lim, __uint_as_float(sq_masked<MODE>()));
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q) wpk[q] = sq_pack<MODE>(__float_as_uint(sv[2 * q]), __float_as_uint(sv[2 * q + 1]));
+      float a0 = l_part * alpha, a1 = 0.0f;
+#pragma unroll
+      for (int q = 0; q < 8; q += 2) {
+        a0 = dot2_ones(wpk[q], a0);
+        a1 = dot2_ones(wpk[q + 1], a1);
+      }
+      l_part = a0 + a1;
+    } else {
+      const float nb1 = __builtin_fmaf(-m_use, p.c1, off);
+#pragma unroll
+      for (int j = 0; j < 16; ++j) sv[j] = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[j], p.c1, nb1));
+      float a[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) a[i] = sv[i] + sv[i + 8];
+#pragma unroll
+      for (int w = 4; w >= 1; w >>= 1)
+#pragma unroll
+        for (int i = 0; i < w; ++i) a[i] = a[i] + a[i + w];
+      l_part = l_part * alpha + a[0];
+    }
+    if (__builtin_amdgcn_ballot_w64(alpha != 1.0f) != 0) {
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) oacc[db][j] *= alpha;
+    }
+
+    // P in the operand type: bf16 as two 16-key operands; fp8 as one 64-key
+    // operand whose other 32 keys (another wave's) carry P = 0
+    bf16x8 pb2[2];
+    i32x8 pf;
+    if constexpr (DT == DT_BF16) {
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        if constexpr (PACKED) {
+          pb2[ks] = __builtin_bit_cast(bf16x8, u32x4{wpk[4 * ks], wpk[4 * ks + 1], wpk[4 * ks + 2], wpk[4 * ks + 3]});
+        } else {
+#pragma unroll
+          for (int r = 0; r < 8; ++r) pb2[ks][r] = (__bf16)sv[8 * ks + r];
+        }
+      }
+    } else {
+      int pw[4];
+#pragma unroll
+      for (int w4 = 0; w4 < 4; ++w4) {
+        if constexpr (PACKED) {
+          i16x2 word = __builtin_bit_cast(i16x2, wpk[2 * w4]);
+          word = __builtin_amdgcn_cvt_scalef32_pk_fp8_bf16(word, __builtin_bit_cast(bf16x2, wpk[2 * w4]), 1.0f, false);
+          word = __builtin_amdgcn_cvt_scalef32_pk_fp8_bf16(word, __builtin_bit_cast(bf16x2, wpk[2 * w4 + 1]), 1.0f,
+                                                           true);
+          pw[w4] = __builtin_bit_cast(int, word);
+        } else {
+          uint32_t word = __float_as_uint(sv[4 * w4]);
+          word = __builtin_amdgcn_cvt_pk_fp8_f32(sv[4 * w4], sv[4 * w4 + 1], word, false);
+          word = __builtin_amdgcn_cvt_pk_fp8_f32(sv[4 * w4 + 2], sv[4 * w4 + 3], word, true);
+          pw[w4] = (int)word;
+        }
+      }
+      if (wave & 1) pf = i32x8{0, 0, 0, 0, pw[0], pw[1], pw[2], pw[3]};
+      else pf = i32x8{pw[0], pw[1], pw[2], pw[3], 0, 0, 0, 0};
+    }
+    if constexpr (PROBE) {
+      if (probe_row) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int key = kw0 + 8 * (j >> 2) + 4 * g + (j & 3);
+          if (key < Sk && key <= limit) {
+            uint32_t bits;
+            if constexpr (DT == DT_BF16) {
+              const u32x4 pw4 = __builtin_bit_cast(u32x4, pb2[j >> 3]);
+              bits = (pw4[(j & 7) >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+            } else {
+              bits = ((uint32_t)pf[4 * (wave & 1) + (j >> 2)] >> (8 * (j & 3))) & 0xFFu;
+            }
+            p.w_out[key] = mode_lattice(MODE) ? __uint_as_float(((wpk[j >> 1] >> (16 * (j & 1))) & 0xFFFFu) << 16)
+                                              : sv[j];
+            p.p_out[key] = bits;
+          }
+        }
+      }
+    }
+
+    // ---- O^T += V^T P^T over this wave's keys
+    set_vbase(vl);
+    if constexpr (DT == DT_BF16) {
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        i32x2v r0 = ds_read_tr16<0>(vbase[db]);
+        i32x2v r1 = ds_read_tr16<8 * C::RB>(vbase[db]);
+        i32x2v r2 = ds_read_tr16<16 * C::RB>(vbase[db]);
+        i32x2v r3 = ds_read_tr16<24 * C::RB>(vbase[db]);
+        lds_wait<0>(r0);
+        lds_wait<0>(r1);
+        lds_wait<0>(r2);
+        lds_wait<0>(r3);
+        const bf16x8 v0 = __builtin_bit_cast(bf16x8, __builtin_shufflevector(r0, r1, 0, 1, 2, 3));
+        const bf16x8 v1 = __builtin_bit_cast(bf16x8, __builtin_shufflevector(r2, r3, 0, 1, 2, 3));
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v0, pb2[0], oacc[db], 0, 0, 0);
+        oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(v1, pb2[1], oacc[db], 0, 0, 0);
+      }
+    } else {
+      const i32x2v zero2 = {0, 0};
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        i32x2v r0 = ds_read_tr8<0>(vbase[db]);
+        i32x2v r1 = ds_read_tr8<16 * C::RB>(vbase[db]);
+        lds_wait<0>(r0);
+        lds_wait<0>(r1);
+        const i32x4 mine = __builtin_shufflevector(r0, r1, 0, 1, 2, 3);
+        const i32x4 none = __builtin_shufflevector(zero2, zero2, 0, 1, 2, 3);
+        const i32x8 vop = (wave & 1) ? __builtin_shufflevector(none, mine, 0, 1, 2, 3, 4, 5, 6, 7)
+                                     : __builtin_shufflevector(mine, none, 0, 1, 2, 3, 4, 5, 6, 7);
+        oacc[db] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vop, pf, oacc[db], 0, 0, 0, 0, 0, 0);
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  }
+
+  // ---- the four waves' partial sums: O^T blocks and row sums through LDS
+  {
+    float la, lb;
+    with_partner(l_part, la, lb);
+    l_lds[wave][lane] = la + lb;
+    float* red = (float*)smem;  // [wave][db][j][lane]
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) red[((wave * NDB + db) * 16 + j) * 64 + lane] = oacc[db][j];
+  }
+  __syncthreads();
+  if (!row_ok) return;
+  const float l = (l_lds[0][lane] + l_lds[1][lane]) + (l_lds[2][lane] + l_lds[3][lane]);
+  if (wave < NDB) {
+    const int db = wave;
+    const float* red = (const float*)smem;
+    f32x16 osum;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      float acc = 0.0f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) acc += red[((w * NDB + db) * 16 + j) * 64 + lane];
+      osum[j] = acc;
+    }
+    if (p.nsplit == 1) {
+      const float inv = p.vd / l;
+      uint16_t* orp = p.o + orow * (size_t)D;
+#pragma unroll
+      for (int jq = 0; jq < 4; ++jq) {
+        const int col = 32 * db + 8 * jq + 4 * g;
+        const __bf16 a0 = (__bf16)(osum[4 * jq + 0] * inv);
+        const __bf16 a1 = (__bf16)(osum[4 * jq + 1] * inv);
+        const __bf16 a2 = (__bf16)(osum[4 * jq + 2] * inv);
+        const __bf16 a3 = (__bf16)(osum[4 * jq + 3] * inv);
+        const uint32_t w01 = (uint32_t)__builtin_bit_cast(uint16_t, a0) |
+                             ((uint32_t)__builtin_bit_cast(uint16_t, a1) << 16);
+        const uint32_t w23 = (uint32_t)__builtin_bit_cast(uint16_t, a2) |
+                             ((uint32_t)__builtin_bit_cast(uint16_t, a3) << 16);
+        *(u32x2*)(orp + col) = u32x2{w01, w23};
+      }
+    } else {
+      float* pop = p.part_o + (orow * (size_t)p.nsplit + (size_t)split) * (size_t)D;
+#pragma unroll
+      for (int jq = 0; jq < 4; ++jq) {
+        const int col = 32 * db + 8 * jq + 4 * g;
+        *(f32x4*)(pop + col) = f32x4{osum[4 * jq], osum[4 * jq + 1], osum[4 * jq + 2], osum[4 * jq + 3]};
+      }
+    }
+  }
+  if (wave == 0 && g == 0) {
+    if (p.nsplit == 1) {
+      if (p.lse) p.lse[orow] = 0.69314718055994531f * (m_run * p.c1 + log2f(l) - off);
+    } else {
+      *(f32x2*)(p.part_ml + (orow * (size_t)p.nsplit + (size_t)split) * 2) = f32x2{m_run, l};
+    }
+  }
+}
+
+struct MergeParams {
+  const float* part_o;
+  const float* part_ml;
+  uint16_t* o;
+  float* lse;
+  int rows, nsplit;
+  float c1, vd, off;
+};
+
+// The parts of each output row merged exactly: m = max m_p, f_p =
+// 2^(c1 (m_p - m)) (0 for a part that saw no key), l = sum f_p l_p,
+// O = sum f_p O_p / l * v_descale, LSE = ln2 (m c1 + log2 l - off).  One wave
+// per row; lane j holds elements j * D / 64 .. of the row.
+template <int D>
+__global__ __launch_bounds__(256) void attn_decode_merge(MergeParams p) {
+  constexpr int E = D / 64;
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= p.rows) return;
+  const float* ml = p.part_ml + (size_t)row * p.nsplit * 2;
+  float m = -INFINITY;
+  for (int s = 0; s < p.nsplit; ++s) m = __builtin_fmaxf(m, ml[2 * s]);
+  float l = 0.0f;
+  float acc[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] = 0.0f;
+  const float* po = p.part_o + (size_t)row * p.nsplit * D + lane * E;
+  for (int s = 0; s < p.nsplit; ++s) {
+    const float ms = ml[2 * s];
+    const float f = ms == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f((ms - m) * p.c1);
+    l += f * ml[2 * s + 1];
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] += f * po[(size_t)s * D + e];
+  }
+  const float inv = p.vd / l;
+  uint16_t* orp = p.o + (size_t)row * D + lane * E;
+#pragma unroll
+  for (int e = 0; e < E; ++e) orp[e] = __builtin_bit_cast(uint16_t, (__bf16)(acc[e] * inv));
+  if (p.lse && lane == 0) p.lse[row] = 0.69314718055994531f * (m * p.c1 + log2f(l) - p.off);
+}
+
+template <int DT, int D, bool CAUSAL, int MODE, bool PROBE>
+hipError_t launch_dec_one(const DecParams& p, hipStream_t st) {
+  const unsigned grid = (unsigned)(p.B * p.Hkv * p.nrb * p.nsplit);
+  hipLaunchKernelGGL((attn_decode_kernel<DT, D, CAUSAL, MODE, PROBE>), dim3(grid), dim3(DEC_NW * 64), 0, st, p);
+  return hipGetLastError();
+}
+
+template <int DT, int D, bool CAUSAL, bool PROBE>
+hipError_t launch_dec_mode(const DecParams& p, int mode, hipStream_t st) {
+  switch (mode) {
+    case MODE_EXACT: return launch_dec_one<DT, D, CAUSAL, MODE_EXACT, PROBE>(p, st);
+    case 1: return launch_dec_one<DT, D, CAUSAL, 1, PROBE>(p, st);
+    case 3: return launch_dec_one<DT, D, CAUSAL, 3, PROBE>(p, st);
+    case 5: return launch_dec_one<DT, D, CAUSAL, 5, PROBE>(p, st);
+    default: break;
+  }
+  if constexpr (DT == DT_FP8) {
+    switch (mode) {
+      case 2: return launch_dec_one<DT, D, CAUSAL, 2, PROBE>(p, st);
+      case 4: return launch_dec_one<DT, D, CAUSAL, 4, PROBE>(p, st);
+      case 6: return launch_dec_one<DT, D, CAUSAL, 6, PROBE>(p, st);
+      default: break;
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+template <bool PROBE>
+hipError_t launch_dec_any(const DecParams& p, int dtype, int d, int causal, int mode, hipStream_t st) {
+  if (dtype == ATTN_BF16) {
+    if (d == 128)
+      return causal ? launch_dec_mode<DT_BF16, 128, true, PROBE>(p, mode, st)
+                    : launch_dec_mode<DT_BF16, 128, false, PROBE>(p, mode, st);
+    return causal ? launch_dec_mode<DT_BF16, 64, true, PROBE>(p, mode, st)
+                  : launch_dec_mode<DT_BF16, 64, false, PROBE>(p, mode, st);
+  }
+  if (d == 128)
+    return causal ? launch_dec_mode<DT_FP8, 128, true, PROBE>(p, mode, st)
+                  : launch_dec_mode<DT_FP8, 128, false, PROBE>(p, mode, st);
+  return causal ? launch_dec_mode<DT_FP8, 64, true, PROBE>(p, mode, st)
+                : launch_dec_mode<DT_FP8, 64, false, PROBE>(p, mode, st);
+}
+
+hipError_t launch_merge(const DecParams& dp, int dtype, int d, hipStream_t st) {
+  MergeParams mp;
+  mp.part_o = dp.part_o;
+  mp.part_ml = dp.part_ml;
+  mp.o = dp.o;
+  mp.lse = dp.lse;
+  mp.rows = dp.B * dp.Hq * dp.Sq;
+  mp.nsplit = dp.nsplit;
+  mp.c1 = dp.c1;
+  mp.vd = dp.vd;
+  mp.off = dtype == ATTN_FP8_E4M3 ? 8.0f : 0.0f;
+  const unsigned grid = (unsigned)((mp.rows + 3) / 4);
+  if (d == 128) hipLaunchKernelGGL(attn_decode_merge<128>, dim3(grid), dim3(256), 0, st, mp);
+  else hipLaunchKernelGGL(attn_decode_merge<64>, dim3(grid), dim3(256), 0, st, mp);
+  return hipGetLastError();
+}
+
 bool finite_pos(float x) { return x > 0.0f && x < INFINITY; }
 
 // Input-rounding order k of an ABI exp_mode (0 for the exact control).
@@ -1120,6 +1661,98 @@ int fill_params(Params& p, const void* q, const void* k, const void* v, void* o,
   return ATTN_OK;
 }
 
+
+// Query rows of one decode workgroup
+constexpr int DEC_ROWS = WROWS;
+
+// Number of key parts for a cut of split_keys keys (0 or >= Sk: one part).
+int dec_parts(int Sk, int split_keys) {
+  if (split_keys <= 0 || split_keys >= Sk) return 1;
+  return (Sk + split_keys - 1) / split_keys;
+}
+
+size_t dec_workspace_bytes(long long rows, int nsplit, int d) {
+  if (nsplit <= 1) return 0;
+  return (size_t)rows * (size_t)nsplit * ((size_t)d + 2) * sizeof(float);
+}
+
+int fill_dec_params(DecParams& p, const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq,
+                    int Hkv, int Sq, int Sk, int Sk_cap, int d, float scale, int dtype, int exp_mode,
+                    int split_keys, const attn_opts* opts) {
+  if (!q || !k || !v || !o) return ATTN_EINVAL;
+  if (B <= 0 || Hq <= 0 || Hkv <= 0 || Sq <= 0 || Sk <= 0 || Sk_cap <= 0 || d <= 0) return ATTN_EINVAL;
+  if (Hq % Hkv != 0 || Sq > Sk || Sk > Sk_cap) return ATTN_EINVAL;
+  if (!finite_pos(scale)) return ATTN_EINVAL;
+  if (split_keys < 0 || split_keys % BC != 0) return ATTN_EINVAL;
+  if (dtype != ATTN_BF16 && dtype != ATTN_FP8_E4M3) return ATTN_EUNSUPPORTED;
+  if (exp_mode != ATTN_EXP_EXACT && exp_order(exp_mode) == 0) return ATTN_EUNSUPPORTED;
+  if (d != 64 && d != 128) return ATTN_EUNSUPPORTED;
+  const uintptr_t mis = (uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)o;
+  if (mis & 15u) return ATTN_EUNSUPPORTED;
+  if (lse && ((uintptr_t)lse & 3u)) return ATTN_EUNSUPPORTED;
+  float qd = 1.0f, kd = 1.0f, vd = 1.0f;
+  if (opts && !(opts->rescale_threshold == 0.0f)) {
+    // the parts take the running maximum as their anchor: threshold 0 only
+    return (opts->rescale_threshold >= 0.0f && opts->rescale_threshold <= 64.0f) ? ATTN_EUNSUPPORTED
+                                                                                  : ATTN_EINVAL;
+  }
+  if (dtype == ATTN_FP8_E4M3) {
+    if (!opts) return ATTN_EINVAL;
+    qd = opts->q_descale;
+    kd = opts->k_descale;
+    vd = opts->v_descale;
+    if (!finite_pos(qd) || !finite_pos(kd) || !finite_pos(vd)) return ATTN_EINVAL;
+  }
+  const long long rows = (long long)B * Hq * Sq;
+  if (rows > (1LL << 30)) return ATTN_EUNSUPPORTED;
+  // one head's cache is addressed with 32-bit byte offsets
+  if ((long long)Sk_cap * d * (dtype == ATTN_BF16 ? 2 : 1) > INT32_MAX) return ATTN_EUNSUPPORTED;
+  const int G = Hq / Hkv;
+  const long long R = (long long)G * Sq;
+  const long long nrb = (R + DEC_ROWS - 1) / DEC_ROWS;
+  const int nsplit = dec_parts(Sk, split_keys);
+  if ((long long)B * Hkv * nrb * nsplit > INT32_MAX) return ATTN_EUNSUPPORTED;
+  p = DecParams{};
+  p.q = (const uint8_t*)q;
+  p.k = (const uint8_t*)k;
+  p.v = (const uint8_t*)v;
+  p.o = (uint16_t*)o;
+  p.lse = lse;
+  p.B = B;
+  p.Hq = Hq;
+  p.Hkv = Hkv;
+  p.Sq = Sq;
+  p.Sk = Sk;
+  p.Sk_cap = Sk_cap;
+  p.G = G;
+  p.R = (int)R;
+  p.nrb = (int)nrb;
+  p.nsplit = nsplit;
+  p.split_keys = nsplit == 1 ? ((Sk + BC - 1) / BC) * BC : split_keys;
+  p.c1 = (float)((double)scale * (double)qd * (double)kd * 1.4426950408889634);
+  p.ck = ldexpf(p.c1, exp_order(exp_mode));
+  p.vd = vd;
+  return ATTN_OK;
+}
+
+// Points the parts' partial results into the workspace (several parts only).
+int bind_workspace(DecParams& p, int d, void* workspace, size_t workspace_bytes) {
+  if (p.nsplit > 1) {
+    const size_t need = dec_workspace_bytes((long long)p.B * p.Hq * p.Sq, p.nsplit, d);
+    if (!workspace || ((uintptr_t)workspace & 15u) || workspace_bytes < need) return ATTN_EINVAL;
+    p.part_o = (float*)workspace;
+    p.part_ml = (float*)workspace + (size_t)p.B * p.Hq * p.Sq * p.nsplit * d;
+  }
+  return ATTN_OK;
+}
+
+int decode_launch(const DecParams& p, int dtype, int d, int causal, int exp_mode, hipStream_t st, bool probe) {
+  const int mode = kernel_mode(dtype, exp_mode, d, p.ck);
+  hipError_t e = probe ? launch_dec_any<true>(p, dtype, d, causal, mode, st)
+                       : launch_dec_any<false>(p, dtype, d, causal, mode, st);
+  if (e == hipSuccess && p.nsplit > 1) e = launch_merge(p, dtype, d, st);
+  return e == hipSuccess ? ATTN_OK : ATTN_ELAUNCH;
+}
 }  // namespace
 
 extern "C" {
@@ -1182,6 +1815,65 @@ int attn_fwd_probe(const void* q, const void* k, const void* v, void* o, float* 
   const int mode = kernel_mode(dtype, exp_mode, d, p.ck);
   const hipError_t e = launch_any<true>(p, dtype, d, causal ? 1 : 0, mode, st);
   return e == hipSuccess ? ATTN_OK : ATTN_ELAUNCH;
+}
+
+int attn_decode_split_keys(int B, int Hq, int Hkv, int Sq, int Sk, int d, int dtype) {
+  (void)d;
+  (void)dtype;
+  if (B <= 0 || Hq <= 0 || Hkv <= 0 || Sq <= 0 || Sk <= 0 || Hq % Hkv != 0) return 0;
+  // aim at two workgroups per compute unit (512), with at least four tiles
+  // of keys per part
+  const long long nrb = ((long long)(Hq / Hkv) * Sq + DEC_ROWS - 1) / DEC_ROWS;
+  const long long groups = (long long)B * Hkv * nrb;
+  const long long tiles = (Sk + BC - 1) / BC;
+  long long parts = (512 + groups - 1) / groups;
+  if (parts > tiles / 4) parts = tiles / 4;
+  if (parts <= 1) return 0;
+  const long long per = (tiles + parts - 1) / parts;
+  return (int)(per * BC);
+}
+
+size_t attn_decode_workspace_bytes(int B, int Hq, int Sq, int Sk, int d, int split_keys) {
+  if (B <= 0 || Hq <= 0 || Sq <= 0 || Sk <= 0 || d <= 0 || split_keys < 0) return 0;
+  return dec_workspace_bytes((long long)B * Hq * Sq, dec_parts(Sk, split_keys), d);
+}
+
+int attn_decode(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq, int Hkv,
+                int Sq, int Sk, int Sk_cap, int d, int causal, float scale, int dtype, int exp_mode,
+                int split_keys, void* workspace, size_t workspace_bytes, const attn_opts* opts) {
+  DecParams p;
+  const int rc = fill_dec_params(p, q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, Sk_cap, d, scale, dtype, exp_mode,
+                                 split_keys, opts);
+  if (rc != ATTN_OK) return rc;
+  const int wrc = bind_workspace(p, d, workspace, workspace_bytes);
+  if (wrc != ATTN_OK) return wrc;
+  hipStream_t st = opts ? (hipStream_t)opts->stream : nullptr;
+  return decode_launch(p, dtype, d, causal ? 1 : 0, exp_mode, st, false);
+}
+
+int attn_decode_probe(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq, int Hkv,
+                      int Sq, int Sk, int Sk_cap, int d, int causal, float scale, int dtype, int exp_mode,
+                      int split_keys, void* workspace, size_t workspace_bytes, const attn_opts* opts, int b,
+                      int h, int i, float* s_out, float* w_out, uint32_t* p_bits_out) {
+  DecParams p;
+  const int rc = fill_dec_params(p, q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, Sk_cap, d, scale, dtype, exp_mode,
+                                 split_keys, opts);
+  if (rc != ATTN_OK) return rc;
+  if (!s_out || !w_out || !p_bits_out) return ATTN_EINVAL;
+  if (b < 0 || b >= B || h < 0 || h >= Hq || i < 0 || i >= Sq) return ATTN_EINVAL;
+  const int wrc = bind_workspace(p, d, workspace, workspace_bytes);
+  if (wrc != ATTN_OK) return wrc;
+  p.pb = b;
+  p.ph = h;
+  p.pi = i;
+  p.s_out = s_out;
+  p.w_out = w_out;
+  p.p_out = p_bits_out;
+  hipStream_t st = opts ? (hipStream_t)opts->stream : nullptr;
+  const size_t n = (size_t)Sk;
+  hipLaunchKernelGGL(probe_fill, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, s_out, w_out, p_bits_out, n);
+  if (hipGetLastError() != hipSuccess) return ATTN_ELAUNCH;
+  return decode_launch(p, dtype, d, causal ? 1 : 0, exp_mode, st, true);
 }
 
 }  // extern "C"

@@ -149,3 +149,26 @@ def make_inputs(B: int, Hq: int, Hkv: int, S: int, d: int, dtype: int, sharp: bo
 
 def workload_inputs(w: Workload) -> Inputs:
     return make_inputs(w.B, w.Hq, w.Hkv, w.S, w.d, w.dtype, w.sharp, w.seed)
+
+
+def make_decode_inputs(B: int, Hq: int, Hkv: int, Sq: int, Sk_cap: int, d: int, dtype: int, sharp: bool,
+                       seed: int) -> Inputs:
+    """Decode inputs: Q [B,Hq,Sq,d] and a key/value cache K, V [B,Hkv,Sk_cap,d],
+    drawn and stored with the same recipe as make_inputs (sharp keys among the
+    cache rows: round(0.02 * Sk_cap) per (b, hkv))."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    q = rng.standard_normal((B, Hq, Sq, d), dtype=np.float32)
+    k = rng.standard_normal((B, Hkv, Sk_cap, d), dtype=np.float32)
+    v = rng.standard_normal((B, Hkv, Sk_cap, d), dtype=np.float32)
+    if sharp:
+        n_sharp = int(round(0.02 * Sk_cap))
+        for b in range(B):
+            for h in range(Hkv):
+                idx = rng.permutation(Sk_cap)[:n_sharp]
+                k[b, h, idx, :] *= np.float32(4.0)
+    if dtype == BF16:
+        return Inputs(bf16_bits(q), bf16_bits(k), bf16_bits(v), (1.0, 1.0, 1.0), BF16)
+    qc, qs = quantize_e4m3(q)
+    kc, ks = quantize_e4m3(k)
+    vc, vs = quantize_e4m3(v)
+    return Inputs(qc, kc, vc, (qs, ks, vs), FP8_E4M3)

@@ -95,3 +95,61 @@ def test_probe_invalid_rows(L):
     for b, h, r0, n in ((1, 0, 0, 1), (0, 2, 0, 1), (0, 0, -1, 1), (0, 0, 0, 0), (0, 0, 60, 5)):
         assert L.attn_fwd_probe(*args, b, h, r0, n, FAKE, FAKE, FAKE) == pkg.ATTN_EINVAL
     assert L.attn_fwd_probe(*args, 0, 0, 0, 4, None, FAKE, FAKE) == pkg.ATTN_EINVAL
+
+
+def test_attn_fwd_accepts_fp8_without_descales(L):
+    # attn_fwd takes FP8 operands at unit descales: an FP8 call passes the
+    # descale check and is stopped only by the size limit checked after it
+    # (B*Hq*S beyond 2^30), before anything is launched; attn_fwd_ex without
+    # options refuses FP8 for want of descales
+    big = [FAKE, FAKE, FAKE, FAKE, None, 8, 2, 1, 1 << 27, 128, 0, 0.1, 1, 1]
+    assert L.attn_fwd(*big) == pkg.ATTN_EUNSUPPORTED
+    assert L.attn_fwd_ex(*big, None) == pkg.ATTN_EINVAL
+    assert L.attn_fwd(None, *big[1:]) == pkg.ATTN_EINVAL
+
+
+def dcall(L, q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=None, B=1, Hq=4, Hkv=2, Sq=1, Sk=1000, cap=1024, d=128,
+          causal=1, scale=0.1, dtype=0, mode=1, split=0, ws=None, wsb=0, opts=None):
+    return L.attn_decode(q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, cap, d, causal, scale, dtype, mode, split, ws, wsb,
+                         ctypes.byref(opts) if opts is not None else None)
+
+
+def test_decode_invalid_arguments(L):
+    E_INV, E_UNS = pkg.ATTN_EINVAL, pkg.ATTN_EUNSUPPORTED
+    assert dcall(L, q=None) == E_INV and dcall(L, o=None) == E_INV
+    for kw in ({"B": 0}, {"Sq": 0}, {"Sk": 0}, {"cap": 0}, {"Hkv": 3}):
+        assert dcall(L, **kw) == E_INV
+    assert dcall(L, Sq=1001) == E_INV          # more query rows than keys
+    assert dcall(L, Sk=1025) == E_INV          # beyond the cache
+    assert dcall(L, split=100) == E_INV and dcall(L, split=-128) == E_INV
+    assert dcall(L, d=96) == E_UNS and dcall(L, mode=pkg.ATTN_EXP_ROWMAX_POT) == E_UNS
+    assert dcall(L, dtype=1) == E_INV          # FP8 needs descales
+    assert dcall(L, opts=pkg.attn_opts(1.0, 1.0, 1.0, None, 8.0, 0)) == E_UNS
+    assert dcall(L, opts=pkg.attn_opts(1.0, 1.0, 1.0, None, -1.0, 0)) == E_INV
+    assert dcall(L, q=FAKE + 8) == E_UNS
+    assert dcall(L, cap=1 << 24, Sk=1 << 23) == E_UNS  # one head's cache beyond 31-bit offsets
+    # several parts need a workspace of the stated size, 16-byte aligned
+    need = pkg.attn_decode_workspace_bytes(1, 4, 1, 1000, 128, 256)
+    assert need == 4 * 1 * 4 * (128 + 2) * 4  # rows x parts x (d + 2) floats
+    assert dcall(L, split=256) == E_INV
+    assert dcall(L, split=256, ws=FAKE, wsb=need - 1) == E_INV
+    assert dcall(L, split=256, ws=FAKE + 4, wsb=need) == E_INV
+    args = [FAKE, FAKE, FAKE, FAKE, None, 1, 4, 2, 2, 1000, 1024, 128, 1, 0.1, 0, 1, 0, None, 0, None]
+    for b, h, i in ((1, 0, 0), (0, 4, 0), (0, 0, 2), (0, 0, -1)):
+        assert L.attn_decode_probe(*args, b, h, i, FAKE, FAKE, FAKE) == E_INV
+    assert L.attn_decode_probe(*args, 0, 0, 0, None, FAKE, FAKE) == E_INV
+
+
+def test_decode_split_and_workspace_sizes(L):
+    assert pkg.attn_decode_workspace_bytes(1, 4, 1, 1000, 128, 0) == 0       # one part
+    assert pkg.attn_decode_workspace_bytes(1, 4, 1, 1000, 128, 1024) == 0    # one part
+    assert pkg.attn_decode_workspace_bytes(2, 8, 3, 1000, 64, 128) == 2 * 8 * 3 * 8 * 66 * 4
+    # the proposed cut: whole tiles, about 512 workgroups, at least four tiles each
+    assert pkg.attn_decode_split_keys(1, 32, 8, 1, 32768, 128, 0) == 512     # 8 groups x 64 parts
+    assert pkg.attn_decode_split_keys(16, 32, 8, 1, 8192, 128, 1) == 2048    # 128 groups x 4 parts
+    assert pkg.attn_decode_split_keys(64, 32, 8, 1, 4096, 128, 0) == 0       # 512 groups: no cut
+    assert pkg.attn_decode_split_keys(1, 8, 8, 1, 600, 128, 0) == 0          # under eight tiles
+    assert pkg.attn_decode_split_keys(0, 8, 8, 1, 600, 128, 0) == 0
+    for args in ((1, 8, 1, 1, 100000, 128, 0), (3, 64, 8, 4, 5000, 64, 1)):
+        s = pkg.attn_decode_split_keys(*args)
+        assert s % 128 == 0 and s >= 0
