@@ -85,7 +85,7 @@ def stratified_rows(B, Hq, S, br, seed):
         qb = int(rng.integers(nqb))
         i = min(qb * br + 32 * (j % nw) + int(rng.integers(32)), S - 1)
         rows.append(j * S + i)
-    for j in rng.choice(B * Hq, 4, replace=False):  # first and last row of query blocks
+    for j in rng.choice(B * Hq, min(4, B * Hq), replace=False):  # first and last row of query blocks
         qb = int(rng.integers(nqb))
         rows += [int(j) * S + qb * br, int(j) * S + min(qb * br + br - 1, S - 1)]
     rows += [0, B * Hq * S - 1]
