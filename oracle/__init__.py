@@ -36,9 +36,12 @@ def lib() -> ctypes.CDLL:
     global _lib
     if _lib is not None:
         return _lib
-    if not LIB_PATH.exists():
+    path = Path(os.environ.get("H15_ORACLE_LIB", "") or LIB_PATH)  # a sanitizer build, when set
+    if not path.exists():
+        if path != LIB_PATH:
+            raise RuntimeError(f"H15_ORACLE_LIB={path} does not exist")
         _build()
-    L = ctypes.CDLL(str(LIB_PATH))
+    L = ctypes.CDLL(str(path))
     c_f, c_d, c_i, c_i64, c_p = ctypes.c_float, ctypes.c_double, ctypes.c_int, ctypes.c_int64, ctypes.c_void_p
     L.oracle_threads.restype = c_i
     L.oracle_bf16_value.argtypes = [ctypes.c_uint16]

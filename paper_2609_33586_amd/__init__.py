@@ -11,6 +11,7 @@ is raised.
 from __future__ import annotations
 
 import ctypes
+import os
 from pathlib import Path
 
 _PKG = Path(__file__).resolve().parent
@@ -41,13 +42,16 @@ _lib = None
 
 
 def lib() -> ctypes.CDLL:
-    """Load libh15attn.so (raises if it has not been built)."""
+    """Load libh15attn.so (raises if it has not been built).  H15ATTN_LIB, when
+    set, names another build of the library to load instead (the host-only
+    sanitizer build of the argument checks)."""
     global _lib
     if _lib is not None:
         return _lib
-    if not LIB_PATH.exists():
-        raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_2609_33586_amd.build.build()")
-    L = ctypes.CDLL(str(LIB_PATH))
+    path = Path(os.environ.get("H15ATTN_LIB", "") or LIB_PATH)
+    if not path.exists():
+        raise RuntimeError(f"{path} is missing: build it with paper_2609_33586_amd.build.build()")
+    L = ctypes.CDLL(str(path))
     P, I, F = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
     common = [P, P, P, P, P, I, I, I, I, I, I, F, I, I]
     L.attn_fwd.argtypes = common

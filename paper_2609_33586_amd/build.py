@@ -17,7 +17,8 @@ from pathlib import Path
 
 PKG = Path(__file__).resolve().parent
 ROOT = PKG.parent
-SRC = PKG / "csrc" / "h15attn.hip"
+SRC = PKG / "csrc" / "h15attn.hip"     # kernels and their launchers
+API_SRC = PKG / "csrc" / "attn_api.cpp"  # C entry points: argument checks, per-call constants
 INCLUDE = ROOT / "include"
 LIB_PATH = PKG / "libh15attn.so"
 ARCH = "gfx950"
@@ -37,11 +38,11 @@ def hipcc() -> str:
 
 def build(extra: list[str] | None = None, verbose: bool = False) -> Path:
     tmp = LIB_PATH.with_name(LIB_PATH.name + ".tmp")
-    cmd = [hipcc(), *HIPCC_FLAGS, *(extra or []), f"-I{INCLUDE}", str(SRC), "-o", str(tmp)]
+    cmd = [hipcc(), *HIPCC_FLAGS, *(extra or []), f"-I{INCLUDE}", str(SRC), str(API_SRC), "-o", str(tmp)]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError(f"hipcc failed ({res.returncode}) building {SRC.name}")
+        raise RuntimeError(f"hipcc failed ({res.returncode}) building {LIB_PATH.name}")
     if verbose:
         sys.stderr.write(res.stderr)
     check_kernel_stubs(tmp)

@@ -30,9 +30,12 @@
 
 #include <type_traits>
 
+#include "attn_params.h"
 #include "h15attn.h"
 
 namespace {
+
+using namespace h15;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -50,8 +53,6 @@ typedef short i16x2 __attribute__((ext_vector_type(2)));
 
 enum { DT_BF16 = 0, DT_FP8 = 1 };
 
-constexpr int WROWS = 32;  // query rows per wave
-constexpr int BC = 128;    // keys per tile (the running max moves once per tile)
 // Waves per workgroup: 4 for FP8 (two workgroups share a CU, so one's
 // barrier and prologue stalls overlap the other's work), 8 for BF16 (whose
 // double-buffered tiles leave LDS for only one workgroup per CU).
@@ -72,36 +73,12 @@ constexpr float H15_MAGIC = 12582912.0f;  // 0x4B400000 = 2^23 + 2^22
 // top half of bits(1.0) in both 16-bit lanes
 constexpr uint32_t ONE_BITS16X2 = 0x3F803F80u;
 
-// Kernel weight modes.  0 is the exact-exp2 control.  The input-rounding
-// family S(Q_{2^-k}) (App. B.2; k = 1 is Rowmax-H15, App. B.1) takes mode
-// 2k - 1 with the clamp in FP32 and 2k with the clamp on the rounded integer
-// in 16-bit lanes (exact only when |y| < 2^15 for every score).  Mode 7 is
-// Rowmax-PoT (App. A.6 Eq. (rowmax-pot)), anchored at the whole-row maximum,
-// BF16 only.
-enum { MODE_EXACT = 0, MODE_H15 = 1, MODE_H15_NARROW = 2, MODE_ROWMAX_POT = 7 };
+// Kernel weight modes (attn_params.h): the order k of a lattice mode, and its
+// clamp form.
 constexpr int mode_order(int mode) { return (mode + 1) / 2; }
 constexpr bool mode_lattice(int mode) { return mode != MODE_EXACT && mode != MODE_ROWMAX_POT; }
 constexpr bool mode_narrow(int mode) { return mode_lattice(mode) && mode % 2 == 0; }
 constexpr int POT_KMAX = 20;  // tail clamp of Rowmax-PoT
-
-struct Params {
-  const uint8_t* q;
-  const uint8_t* k;
-  const uint8_t* v;
-  uint16_t* o;
-  float* lse;
-  int B, Hq, Hkv, S, G;
-  float c1, ck, vd;  // base-two logit scale; 2^k c1 for the weight; V descale
-  float tau;          // conditional-rescale threshold (0: the anchor is the running max)
-  int tau_wave;       // 1: the anchor decision is shared by the wave's 32 rows
-  int nqb;    // query blocks per head
-  int remap;  // XCD-grouped workgroup order: 0 none, 1 query blocks outermost, 2 KV heads outermost
-  // probe target (PROBE instantiations only)
-  int pb, ph, prow0, pnrows;
-  float* s_out;
-  float* w_out;
-  uint32_t* p_out;
-};
 
 template <int DT, int D>
 struct Cfg {
@@ -114,6 +91,7 @@ struct Cfg {
   static constexpr int NW = waves_per_group<DT>();  // waves per workgroup
   static constexpr int BR = NW * WROWS;             // query rows per workgroup
   static_assert(CHUNKS % (NW * 64) == 0, "tile/staging mismatch");
+  static_assert(BR == (DT == DT_FP8 ? FWD_ROWS_FP8 : FWD_ROWS_BF16), "row block of attn_params.h");
 };
 
 // Bank-spreading XOR swizzles of the 16-byte chunks of a row.  K rows are read
@@ -1052,23 +1030,6 @@ hipError_t launch_any(const Params& p, int dtype, int d, int causal, int mode, h
 // waves' partial row sums and O accumulators, all relative to that maximum,
 // are added up at the end.
 
-struct DecParams {
-  const uint8_t* q;
-  const uint8_t* k;
-  const uint8_t* v;
-  uint16_t* o;
-  float* lse;
-  float* part_o;   // [rows][nsplit][d], unnormalised O of each part (nsplit > 1)
-  float* part_ml;  // [rows][nsplit][2], (m, l) of each part (nsplit > 1)
-  int B, Hq, Hkv, Sq, Sk, Sk_cap, G, R, nrb, nsplit, split_keys;
-  float c1, ck, vd;
-  // probe target (PROBE instantiations only): output row (pb, ph, pi)
-  int pb, ph, pi;
-  float* s_out;
-  float* w_out;
-  uint32_t* p_out;
-};
-
 constexpr int DEC_NW = 4;  // waves per decode workgroup (one 32-key block each)
 
 __device__ __forceinline__ void settle_block(f32x16& v) {
@@ -1572,308 +1533,29 @@ hipError_t launch_merge(const DecParams& dp, int dtype, int d, hipStream_t st) {
   return hipGetLastError();
 }
 
-bool finite_pos(float x) { return x > 0.0f && x < INFINITY; }
+}  // namespace
 
-// Input-rounding order k of an ABI exp_mode (0 for the exact control).
-int exp_order(int exp_mode) {
-  switch (exp_mode) {
-    case ATTN_EXP_H15: return 1;
-    case ATTN_EXP_SQ4: return 2;
-    case ATTN_EXP_SQ8: return 3;
-    default: return 0;
-  }
+namespace h15 {
+
+int launch_fwd(const Params& p, int dtype, int d, int causal, int mode, void* stream, bool probe) {
+  hipStream_t st = (hipStream_t)stream;
+  const hipError_t e = probe ? launch_any<true>(p, dtype, d, causal, mode, st)
+                             : launch_any<false>(p, dtype, d, causal, mode, st);
+  return e == hipSuccess ? 0 : 1;
 }
 
-// Kernel variant for an ABI exp_mode.  For FP8 every raw logit satisfies
-// |s| <= d * 448^2, so |y| <= 2 ck d 448^2 + 8 * 2^k with ck = 2^k c1; when
-// that is below 2^15 the rounded integer n = RNE(y) fits an int16 lane and
-// the clamp can be taken there (the narrow mode).
-int kernel_mode(int dtype, int exp_mode, int d, float ck) {
-  if (exp_mode == ATTN_EXP_ROWMAX_POT) return MODE_ROWMAX_POT;
-  const int k = exp_order(exp_mode);
-  if (k == 0) return MODE_EXACT;
-  if (dtype == ATTN_FP8_E4M3) {
-    const double ymax = 2.0 * (double)ck * (double)d * 448.0 * 448.0 * (1.0 + 1e-5) + 8.0 * (1 << k);
-    if (ymax < 32767.0) return 2 * k;
-  }
-  return 2 * k - 1;
+int launch_probe_fill(float* s, float* w, uint32_t* pbits, size_t n, void* stream) {
+  hipLaunchKernelGGL(probe_fill, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, (hipStream_t)stream, s, w, pbits,
+                     n);
+  return hipGetLastError() == hipSuccess ? 0 : 1;
 }
 
-// query rows per workgroup for an operand type
-int row_block(int dtype) {
-  return (dtype == ATTN_FP8_E4M3 ? Cfg<DT_FP8, 128>::BR : Cfg<DT_BF16, 128>::BR);
-}
-
-int fill_params(Params& p, const void* q, const void* k, const void* v, void* o, float* lse, int B,
-                int Hq, int Hkv, int S, int d, float scale, int dtype, int exp_mode,
-                const attn_opts* opts) {
-  if (!q || !k || !v || !o) return ATTN_EINVAL;
-  if (B <= 0 || Hq <= 0 || Hkv <= 0 || S <= 0 || d <= 0) return ATTN_EINVAL;
-  if (Hq % Hkv != 0) return ATTN_EINVAL;
-  if (!finite_pos(scale)) return ATTN_EINVAL;
-  if (dtype != ATTN_BF16 && dtype != ATTN_FP8_E4M3) return ATTN_EUNSUPPORTED;
-  if (exp_mode != ATTN_EXP_EXACT && exp_mode != ATTN_EXP_ROWMAX_POT && exp_order(exp_mode) == 0)
-    return ATTN_EUNSUPPORTED;
-  // Rowmax-PoT: 21 levels 2^0 .. 2^-20 need bf16's range for P (e4m3 spans
-  // under 18 octaves); its anchor is the whole-row maximum, so no threshold
-  if (exp_mode == ATTN_EXP_ROWMAX_POT && (dtype != ATTN_BF16 || (opts && opts->rescale_threshold != 0.0f)))
-    return ATTN_EUNSUPPORTED;
-  if (d != 64 && d != 128) return ATTN_EUNSUPPORTED;
-  const uintptr_t mis = (uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)o;
-  if (mis & 15u) return ATTN_EUNSUPPORTED;
-  if (lse && ((uintptr_t)lse & 3u)) return ATTN_EUNSUPPORTED;
-  float qd = 1.0f, kd = 1.0f, vd = 1.0f;
-  const float tau = opts ? opts->rescale_threshold : 0.0f;
-  if (!(tau >= 0.0f && tau <= 64.0f)) return ATTN_EINVAL;
-  if (dtype == ATTN_FP8_E4M3) {
-    if (!opts) return ATTN_EINVAL;
-    if (tau != 0.0f) return ATTN_EUNSUPPORTED;
-    qd = opts->q_descale;
-    kd = opts->k_descale;
-    vd = opts->v_descale;
-    if (!finite_pos(qd) || !finite_pos(kd) || !finite_pos(vd)) return ATTN_EINVAL;
-  }
-  const long long rows = (long long)B * Hq * S;
-  if (rows > (1LL << 31) / 2) return ATTN_EUNSUPPORTED;
-  // one head's K or V rows are addressed with 32-bit byte offsets
-  if ((long long)S * d * (dtype == ATTN_BF16 ? 2 : 1) > INT32_MAX) return ATTN_EUNSUPPORTED;
-  p = Params{};
-  p.q = (const uint8_t*)q;
-  p.k = (const uint8_t*)k;
-  p.v = (const uint8_t*)v;
-  p.o = (uint16_t*)o;
-  p.lse = lse;
-  p.B = B;
-  p.Hq = Hq;
-  p.Hkv = Hkv;
-  p.S = S;
-  p.G = Hq / Hkv;
-  // base-two exponent scale of a raw logit; the weight uses 2^k times it
-  // (the doubled constant of App. B.1 for k = 1; the scaling is exact), the
-  // rescale factor and LSE the plain one
-  p.c1 = (float)((double)scale * (double)qd * (double)kd * 1.4426950408889634);
-  p.ck = ldexpf(p.c1, exp_order(exp_mode));
-  p.vd = vd;
-  p.tau = tau;
-  p.tau_wave = (opts && opts->rescale_per_wave) ? 1 : 0;
-  p.nqb = (S + row_block(dtype) - 1) / row_block(dtype);
-  p.remap = ((B * Hkv) % 8 == 0) ? 1 : 0;
-  return ATTN_OK;
-}
-
-
-// Query rows of one decode workgroup
-constexpr int DEC_ROWS = WROWS;
-
-// Number of key parts for a cut of split_keys keys (0 or >= Sk: one part).
-int dec_parts(int Sk, int split_keys) {
-  if (split_keys <= 0 || split_keys >= Sk) return 1;
-  return (Sk + split_keys - 1) / split_keys;
-}
-
-size_t dec_workspace_bytes(long long rows, int nsplit, int d) {
-  if (nsplit <= 1) return 0;
-  return (size_t)rows * (size_t)nsplit * ((size_t)d + 2) * sizeof(float);
-}
-
-int fill_dec_params(DecParams& p, const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq,
-                    int Hkv, int Sq, int Sk, int Sk_cap, int d, float scale, int dtype, int exp_mode,
-                    int split_keys, const attn_opts* opts) {
-  if (!q || !k || !v || !o) return ATTN_EINVAL;
-  if (B <= 0 || Hq <= 0 || Hkv <= 0 || Sq <= 0 || Sk <= 0 || Sk_cap <= 0 || d <= 0) return ATTN_EINVAL;
-  if (Hq % Hkv != 0 || Sq > Sk || Sk > Sk_cap) return ATTN_EINVAL;
-  if (!finite_pos(scale)) return ATTN_EINVAL;
-  if (split_keys < 0 || split_keys % BC != 0) return ATTN_EINVAL;
-  if (dtype != ATTN_BF16 && dtype != ATTN_FP8_E4M3) return ATTN_EUNSUPPORTED;
-  if (exp_mode != ATTN_EXP_EXACT && exp_order(exp_mode) == 0) return ATTN_EUNSUPPORTED;
-  if (d != 64 && d != 128) return ATTN_EUNSUPPORTED;
-  const uintptr_t mis = (uintptr_t)q | (uintptr_t)k | (uintptr_t)v | (uintptr_t)o;
-  if (mis & 15u) return ATTN_EUNSUPPORTED;
-  if (lse && ((uintptr_t)lse & 3u)) return ATTN_EUNSUPPORTED;
-  float qd = 1.0f, kd = 1.0f, vd = 1.0f;
-  if (opts && !(opts->rescale_threshold == 0.0f)) {
-    // the parts take the running maximum as their anchor: threshold 0 only
-    return (opts->rescale_threshold >= 0.0f && opts->rescale_threshold <= 64.0f) ? ATTN_EUNSUPPORTED
-                                                                                  : ATTN_EINVAL;
-  }
-  if (dtype == ATTN_FP8_E4M3) {
-    if (!opts) return ATTN_EINVAL;
-    qd = opts->q_descale;
-    kd = opts->k_descale;
-    vd = opts->v_descale;
-    if (!finite_pos(qd) || !finite_pos(kd) || !finite_pos(vd)) return ATTN_EINVAL;
-  }
-  const long long rows = (long long)B * Hq * Sq;
-  if (rows > (1LL << 30)) return ATTN_EUNSUPPORTED;
-  // one head's cache is addressed with 32-bit byte offsets
-  if ((long long)Sk_cap * d * (dtype == ATTN_BF16 ? 2 : 1) > INT32_MAX) return ATTN_EUNSUPPORTED;
-  const int G = Hq / Hkv;
-  const long long R = (long long)G * Sq;
-  const long long nrb = (R + DEC_ROWS - 1) / DEC_ROWS;
-  const int nsplit = dec_parts(Sk, split_keys);
-  if ((long long)B * Hkv * nrb * nsplit > INT32_MAX) return ATTN_EUNSUPPORTED;
-  p = DecParams{};
-  p.q = (const uint8_t*)q;
-  p.k = (const uint8_t*)k;
-  p.v = (const uint8_t*)v;
-  p.o = (uint16_t*)o;
-  p.lse = lse;
-  p.B = B;
-  p.Hq = Hq;
-  p.Hkv = Hkv;
-  p.Sq = Sq;
-  p.Sk = Sk;
-  p.Sk_cap = Sk_cap;
-  p.G = G;
-  p.R = (int)R;
-  p.nrb = (int)nrb;
-  p.nsplit = nsplit;
-  p.split_keys = nsplit == 1 ? ((Sk + BC - 1) / BC) * BC : split_keys;
-  p.c1 = (float)((double)scale * (double)qd * (double)kd * 1.4426950408889634);
-  p.ck = ldexpf(p.c1, exp_order(exp_mode));
-  p.vd = vd;
-  return ATTN_OK;
-}
-
-// Points the parts' partial results into the workspace (several parts only).
-int bind_workspace(DecParams& p, int d, void* workspace, size_t workspace_bytes) {
-  if (p.nsplit > 1) {
-    const size_t need = dec_workspace_bytes((long long)p.B * p.Hq * p.Sq, p.nsplit, d);
-    if (!workspace || ((uintptr_t)workspace & 15u) || workspace_bytes < need) return ATTN_EINVAL;
-    p.part_o = (float*)workspace;
-    p.part_ml = (float*)workspace + (size_t)p.B * p.Hq * p.Sq * p.nsplit * d;
-  }
-  return ATTN_OK;
-}
-
-int decode_launch(const DecParams& p, int dtype, int d, int causal, int exp_mode, hipStream_t st, bool probe) {
-  const int mode = kernel_mode(dtype, exp_mode, d, p.ck);
+int launch_decode(const DecParams& p, int dtype, int d, int causal, int mode, void* stream, bool probe) {
+  hipStream_t st = (hipStream_t)stream;
   hipError_t e = probe ? launch_dec_any<true>(p, dtype, d, causal, mode, st)
                        : launch_dec_any<false>(p, dtype, d, causal, mode, st);
   if (e == hipSuccess && p.nsplit > 1) e = launch_merge(p, dtype, d, st);
-  return e == hipSuccess ? ATTN_OK : ATTN_ELAUNCH;
-}
-}  // namespace
-
-extern "C" {
-
-int attn_tile_bc(void) { return BC; }
-
-const char* attn_strerror(int code) {
-  switch (code) {
-    case ATTN_OK: return "ok";
-    case ATTN_EINVAL: return "invalid argument";
-    case ATTN_EUNSUPPORTED: return "unsupported configuration";
-    case ATTN_ELAUNCH: return "kernel launch failed";
-    default: return "unknown error code";
-  }
+  return e == hipSuccess ? 0 : 1;
 }
 
-int attn_fwd_ex(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq,
-                int Hkv, int S, int d, int causal, float scale, int dtype, int exp_mode,
-                const attn_opts* opts) {
-  Params p;
-  const int rc = fill_params(p, q, k, v, o, lse, B, Hq, Hkv, S, d, scale, dtype, exp_mode, opts);
-  if (rc != ATTN_OK) return rc;
-  if (p.remap && !causal) p.remap = 2;
-  hipStream_t st = opts ? (hipStream_t)opts->stream : nullptr;
-  const int mode = kernel_mode(dtype, exp_mode, d, p.ck);
-  const hipError_t e = launch_any<false>(p, dtype, d, causal ? 1 : 0, mode, st);
-  return e == hipSuccess ? ATTN_OK : ATTN_ELAUNCH;
-}
-
-int attn_fwd(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq,
-             int Hkv, int S, int d, int causal, float scale, int dtype, int exp_mode) {
-  // unit descales (FP8 values are taken as stored), default stream, threshold 0
-  const attn_opts unit = {1.0f, 1.0f, 1.0f, nullptr, 0.0f, 0};
-  return attn_fwd_ex(q, k, v, o, lse, B, Hq, Hkv, S, d, causal, scale, dtype, exp_mode, &unit);
-}
-
-int attn_fwd_probe(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq,
-                   int Hkv, int S, int d, int causal, float scale, int dtype, int exp_mode,
-                   const attn_opts* opts, int b, int h, int row0, int nrows, float* s_out,
-                   float* w_out, uint32_t* p_bits_out) {
-  Params p;
-  const int rc = fill_params(p, q, k, v, o, lse, B, Hq, Hkv, S, d, scale, dtype, exp_mode, opts);
-  if (rc != ATTN_OK) return rc;
-  if (p.remap && !causal) p.remap = 2;
-  if (!s_out || !w_out || !p_bits_out) return ATTN_EINVAL;
-  if (b < 0 || b >= B || h < 0 || h >= Hq || row0 < 0 || nrows < 1 || row0 + nrows > S)
-    return ATTN_EINVAL;
-  p.pb = b;
-  p.ph = h;
-  p.prow0 = row0;
-  p.pnrows = nrows;
-  p.s_out = s_out;
-  p.w_out = w_out;
-  p.p_out = p_bits_out;
-  hipStream_t st = opts ? (hipStream_t)opts->stream : nullptr;
-  const size_t n = (size_t)nrows * (size_t)S;
-  hipLaunchKernelGGL(probe_fill, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, s_out, w_out,
-                     p_bits_out, n);
-  if (hipGetLastError() != hipSuccess) return ATTN_ELAUNCH;
-  const int mode = kernel_mode(dtype, exp_mode, d, p.ck);
-  const hipError_t e = launch_any<true>(p, dtype, d, causal ? 1 : 0, mode, st);
-  return e == hipSuccess ? ATTN_OK : ATTN_ELAUNCH;
-}
-
-int attn_decode_split_keys(int B, int Hq, int Hkv, int Sq, int Sk, int d, int dtype) {
-  (void)d;
-  (void)dtype;
-  if (B <= 0 || Hq <= 0 || Hkv <= 0 || Sq <= 0 || Sk <= 0 || Hq % Hkv != 0) return 0;
-  // aim at two workgroups per compute unit (512), with at least four tiles
-  // of keys per part
-  const long long nrb = ((long long)(Hq / Hkv) * Sq + DEC_ROWS - 1) / DEC_ROWS;
-  const long long groups = (long long)B * Hkv * nrb;
-  const long long tiles = (Sk + BC - 1) / BC;
-  long long parts = (512 + groups - 1) / groups;
-  if (parts > tiles / 4) parts = tiles / 4;
-  if (parts <= 1) return 0;
-  const long long per = (tiles + parts - 1) / parts;
-  return (int)(per * BC);
-}
-
-size_t attn_decode_workspace_bytes(int B, int Hq, int Sq, int Sk, int d, int split_keys) {
-  if (B <= 0 || Hq <= 0 || Sq <= 0 || Sk <= 0 || d <= 0 || split_keys < 0) return 0;
-  return dec_workspace_bytes((long long)B * Hq * Sq, dec_parts(Sk, split_keys), d);
-}
-
-int attn_decode(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq, int Hkv,
-                int Sq, int Sk, int Sk_cap, int d, int causal, float scale, int dtype, int exp_mode,
-                int split_keys, void* workspace, size_t workspace_bytes, const attn_opts* opts) {
-  DecParams p;
-  const int rc = fill_dec_params(p, q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, Sk_cap, d, scale, dtype, exp_mode,
-                                 split_keys, opts);
-  if (rc != ATTN_OK) return rc;
-  const int wrc = bind_workspace(p, d, workspace, workspace_bytes);
-  if (wrc != ATTN_OK) return wrc;
-  hipStream_t st = opts ? (hipStream_t)opts->stream : nullptr;
-  return decode_launch(p, dtype, d, causal ? 1 : 0, exp_mode, st, false);
-}
-
-int attn_decode_probe(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq, int Hkv,
-                      int Sq, int Sk, int Sk_cap, int d, int causal, float scale, int dtype, int exp_mode,
-                      int split_keys, void* workspace, size_t workspace_bytes, const attn_opts* opts, int b,
-                      int h, int i, float* s_out, float* w_out, uint32_t* p_bits_out) {
-  DecParams p;
-  const int rc = fill_dec_params(p, q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, Sk_cap, d, scale, dtype, exp_mode,
-                                 split_keys, opts);
-  if (rc != ATTN_OK) return rc;
-  if (!s_out || !w_out || !p_bits_out) return ATTN_EINVAL;
-  if (b < 0 || b >= B || h < 0 || h >= Hq || i < 0 || i >= Sq) return ATTN_EINVAL;
-  const int wrc = bind_workspace(p, d, workspace, workspace_bytes);
-  if (wrc != ATTN_OK) return wrc;
-  p.pb = b;
-  p.ph = h;
-  p.pi = i;
-  p.s_out = s_out;
-  p.w_out = w_out;
-  p.p_out = p_bits_out;
-  hipStream_t st = opts ? (hipStream_t)opts->stream : nullptr;
-  const size_t n = (size_t)Sk;
-  hipLaunchKernelGGL(probe_fill, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, s_out, w_out, p_bits_out, n);
-  if (hipGetLastError() != hipSuccess) return ATTN_ELAUNCH;
-  return decode_launch(p, dtype, d, causal ? 1 : 0, exp_mode, st, true);
-}
-
-}  // extern "C"
+}  // namespace h15
