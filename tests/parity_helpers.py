@@ -131,6 +131,10 @@ def lse_bound_lattice(s, qrow, krows, jend, i, causal, c1, dt, k, Bc, lse_ref):
             + 4.0 * float(np.spacing(np.float32(abs(lse_ref)))) + 1e-6)
 
 
+# the constant terms of lse_bound_lattice for one tile (no ulps)
+LSE_FLOOR = 67 * 2.0 ** -24 + 1e-6
+
+
 def lse_bounds(inp, rows, causal, sc, mode):
     """lse_bound_lattice for each flat row (b * Hq + h) * S + i of a square problem."""
     B, Hq, S, d = inp.q.shape
@@ -171,9 +175,16 @@ def assert_close(inp, o, lse, o_ref, lse_ref, what, mode=EXACT, causal=None, sc=
         assert causal is not None and sc is not None, "the lattice LSE bound needs the mask and the scale"
         if rows is None:
             rows = np.arange(lse.shape[0])
-        lb = lse_bounds(inp, rows, causal, sc, mode)
+        rows = np.asarray(rows)
+        # every row's bound is at least its constant terms ((3 + 64) 2^-24 +
+        # 1e-6 + four ulps of |LSE|); rows that agree that closely pass
+        # whatever their bound, so it is computed only for the others
+        lb = LSE_FLOOR + 4.0 * np.spacing(np.abs(lse_ref).astype(np.float32)).astype(np.float64)
+        above = dl_raw > lb
+        if np.any(above):
+            lb[above] = lse_bounds(inp, rows[above], causal, sc, mode)
         worst = int(np.argmax(dl_raw - lb))
-        say(f"  {what}: LSE within the per-row bound (median bound {np.median(lb):.2e}, "
+        say(f"  {what}: LSE within the per-row bound ({int(np.sum(above))} of {len(rows)} rows above its floor, "
             f"worst margin {float(lb[worst] - dl_raw[worst]):.2e})")
         assert np.all(dl_raw <= lb), f"{what}: row {rows[worst]} |dLSE| {dl_raw[worst]:.3e} > {lb[worst]:.3e}"
         # the bound takes every weight within reach to move the same way; in
