@@ -40,6 +40,8 @@ def parse():
                     help="calls per timed window; the windows of the timed variants alternate")
     ap.add_argument("--no-noncausal", action="store_true",
                     help="do not time the non-causal FP8 8K H15/exact pair beside the default workload")
+    ap.add_argument("--no-decode", action="store_true",
+                    help="do not time decode over a key/value cache (B16 Hq32 Hkv8, one query row, 8K cache)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU baseline sample time")
     ap.add_argument("--modes", default=None,
@@ -122,6 +124,63 @@ def time_modes(pkg, torch, q, k, v, inp, causal, scale, modes, warmup=10, rounds
             torch.cuda.synchronize()
             res[name].append(e0.elapsed_time(e1) / per_window)
     return {name: float(np.median(v)) for name, v in res.items()}
+
+
+# Decode benchmark shape: 16 sequences, 32 query heads over 8 key/value heads,
+# one new query row per head against an 8K-entry cache, d = 128.
+DECODE_SHAPE = (16, 32, 8, 1, 8192, 128)
+HBM_PEAK_GBPS = 8000.0
+
+
+def decode_bench(torch, pkg, synth, stream, steps=200, warmup=50, window=25):
+    """Decode (attn_decode, the library's proposed key cut) in FP8 and BF16,
+    H15 and the exact control in alternating windows.  The calls go straight
+    to the C entry point with their arguments marshalled once, so the timing
+    is the kernels' (parts + merge), not Python's.  Bytes per call: the K/V
+    cache rows read, Q read, O and LSE written (the parts' partial results in
+    the workspace are reported separately)."""
+    import ctypes
+    B, Hq, Hkv, Sq, Sk, d = DECODE_SHAPE
+    L = pkg.lib()
+    scale = float(np.float32(1.0 / math.sqrt(d)))
+    res = {"workload": f"decode_b{B}_h{Hq}kv{Hkv}_sq{Sq}_sk{Sk}_d{d}_sharp", "shape":
+           {"B": B, "Hq": Hq, "Hkv": Hkv, "Sq": Sq, "Sk": Sk, "d": d, "causal": True}}
+    calls, meta, keep = {}, {}, []
+    for dtn, dt in (("fp8", synth.FP8_E4M3), ("bf16", synth.BF16)):
+        inp = synth.make_decode_inputs(B, Hq, Hkv, Sq, Sk, d, dt, sharp=True, seed=1800 + dt)
+        q, k, v = device_tensors(inp, torch)
+        split = pkg.attn_decode_split_keys(B, Hq, Hkv, Sq, Sk, d, dt)
+        ws_bytes = pkg.attn_decode_workspace_bytes(B, Hq, Sq, Sk, d, split)
+        ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=q.device)
+        o = torch.empty((B, Hq, Sq, d), dtype=torch.bfloat16, device=q.device)
+        lse = torch.empty((B, Hq, Sq), dtype=torch.float32, device=q.device)
+        opts = pkg.attn_opts(*inp.descale, ctypes.c_void_p(stream.cuda_stream))
+        keep += [q, k, v, ws, o, lse, opts]
+        eb = 1 if dt == synth.FP8_E4M3 else 2
+        meta[dtn] = {"split_keys": split, "parts": -(-Sk // split) if split else 1, "workspace_bytes": ws_bytes,
+                     "bytes_per_call": B * Hkv * Sk * d * eb * 2 + B * Hq * Sq * d * eb + B * Hq * Sq * (2 * d + 4)}
+        for mn, mode in (("h15", pkg.ATTN_EXP_H15), ("exact", pkg.ATTN_EXP_EXACT)):
+            args = (q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), lse.data_ptr(), B, Hq, Hkv, Sq, Sk, Sk,
+                    d, 1, scale, dt, mode, split, ws.data_ptr(), ws_bytes, ctypes.byref(opts))
+            rc = L.attn_decode(*args)
+            if rc != pkg.ATTN_OK:
+                raise pkg.AttnError(rc, "attn_decode")
+            calls[f"{dtn}_{mn}"] = (lambda a=args: L.attn_decode(*a))
+    windows = timed_windows(torch, stream, calls, steps, warmup, window)
+    for dtn in ("fp8", "bf16"):
+        us = {}
+        for mn in ("h15", "exact"):
+            w = windows[f"{dtn}_{mn}"]
+            us[mn] = float(np.median([t / n for t, n in w])) * 1e3
+        nb = meta[dtn]["bytes_per_call"]
+        gbps = nb / (us["h15"] * 1e-6) / 1e9
+        res[dtn] = {**meta[dtn], "h15_us_per_call": round(us["h15"], 2), "exact_us_per_call": round(us["exact"], 2),
+                    "h15_GBps": round(gbps, 1), "h15_hbm_frac": round(gbps / HBM_PEAK_GBPS, 4),
+                    "exact_GBps": round(nb / (us["exact"] * 1e-6) / 1e9, 1),
+                    "h15_vs_exact_speedup_pct": round(100.0 * (us["exact"] / us["h15"] - 1.0), 2)}
+    res["estimator"] = f"median window of {window} back-to-back calls, {steps} timed calls per variant"
+    del keep
+    return res
 
 
 def timed_windows(torch, stream, calls, steps, warmup, window):
@@ -411,6 +470,9 @@ def main():
         line["weight_variants"] = {
             m: {"ms_per_call": round(res_ms[m], 5), "tflops": round(tflops[m], 2),
                 "vs_h15_pct": round(100.0 * (res_ms["h15"] / res_ms[m] - 1.0), 2)} for m in variants}
+    if args.workload == DEFAULT_WORKLOAD and not args.no_decode:
+        # decode over a key/value cache: HBM-bound (the cache is read once)
+        line["decode"] = decode_bench(torch, pkg, synth, stream)
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(w, inp, scale, args.cpu_seconds)
     print(json.dumps(line), flush=True)

@@ -398,8 +398,14 @@ def test_rowmax_pot_full_size(w):
 @pytest.mark.parametrize("mode", [EXACT, H15])
 def test_attn_fwd_fp8_takes_unit_descales(mode):
     # attn_fwd has no descale arguments: FP8 operands are taken as stored,
-    # the same as attn_fwd_ex with descales (1, 1, 1)
-    inp = synth.make_inputs(1, 4, 2, 300, 128, FP8, sharp=True, seed=990)
+    # the same as attn_fwd_ex with descales (1, 1, 1).  The operands are
+    # encoded at unit scale (Gaussian values, |x| < 5, as e4m3 codes), so the
+    # real logits keep the size the LSE bar assumes; the launcher still takes
+    # the FP32 clamp, its exponent bound at unit descales being far above 2^15
+    base = synth.make_inputs(1, 4, 2, 300, 128, FP8, sharp=True, seed=990)
+    rng = np.random.default_rng(990)
+    codes = [synth.e4m3_codes(rng.standard_normal(x.shape).astype(np.float32)) for x in (base.q, base.k, base.v)]
+    inp = synth.Inputs(*codes, (1.0, 1.0, 1.0), FP8)
     q, k, v = dev_tensors(inp)
     sc = scale_of(128)
     o1, l1 = pkg.attn_fwd(q, k, v, causal=True, scale=sc, exp_mode=mode)
