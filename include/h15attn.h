@@ -58,7 +58,8 @@
  * the library allocates, frees and synchronises nothing.  Calls are
  * asynchronous on the given stream (NULL: the default stream); buffers must
  * stay valid until the stream reaches the work.  The library holds no state
- * and may be called from several threads.
+ * and may be called from several threads, except for the built-in decode
+ * workspace of attn_decode_noalloc (one buffer per GPU, shared by its calls).
  *
  * Errors: arguments are validated before anything is launched; on error
  * nothing is written.  Every entry point returns ATTN_OK or a negative code,
@@ -91,7 +92,10 @@ enum attn_status {
                               pointer not 16-byte aligned, B*Hq*S > 2^30, or
                               one head's K/V rows (S * d * element bytes)
                               not addressable with 31-bit offsets */
-    ATTN_ELAUNCH = -3      /* the HIP launch reported an error */
+    ATTN_ELAUNCH = -3,     /* the HIP runtime reported an error (a launch, or
+                              naming the device for attn_decode_noalloc) */
+    ATTN_ENOSPACE = -4     /* attn_decode_noalloc: the cut needs more workspace
+                              than the built-in buffer holds */
 };
 
 /* Optional per-call settings.  FP8 requires the three per-tensor descales
@@ -201,6 +205,27 @@ size_t attn_decode_workspace_bytes(int B, int Hq, int Sq, int Sk, int d, int spl
  * the shape fills the GPU without cutting.  A function of its arguments
  * only; 0 for invalid sizes. */
 int attn_decode_split_keys(int B, int Hq, int Hkv, int Sq, int Sk, int d, int dtype);
+
+/* attn_decode for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same kernels and results as attn_decode with the same split_keys, but
+ * the parts' partial results go to a workspace built into the library, one
+ * 16 MiB buffer per GPU (allocated when the library's code is loaded on that
+ * GPU and held until the process ends), instead of a caller's buffer.  The
+ * call allocates and frees nothing.  Every call on one GPU shares that GPU's
+ * buffer: calls that may overlap on one GPU (other streams, other threads)
+ * race and give wrong results; calls in stream order are safe.  Nothing in
+ * the buffer needs clearing (every part writes all of its partial results
+ * before the merge reads them).  The first call on a device looks up that
+ * device's buffer with the device current.
+ *
+ * Errors: those of attn_decode (without the workspace ones), and
+ * ATTN_ENOSPACE when attn_decode_workspace_bytes() of the shape and cut
+ * exceeds 16 MiB (16777216 bytes; choose a coarser cut, or use attn_decode);
+ * nothing is launched then. */
+int attn_decode_noalloc(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq, int Hkv,
+                        int Sq, int Sk, int Sk_cap, int d, int causal, float scale, int dtype, int exp_mode,
+                        int split_keys, const attn_opts* opts);
 
 /* Test access to decode's intermediate values, as attn_fwd_probe: runs the
  * same kernels as attn_decode (O and LSE written identically) and stores, for

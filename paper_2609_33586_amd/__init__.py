@@ -19,11 +19,11 @@ LIB_PATH = _PKG / "libh15attn.so"
 
 ATTN_BF16, ATTN_FP8_E4M3 = 0, 1
 ATTN_EXP_EXACT, ATTN_EXP_H15, ATTN_EXP_SQ4, ATTN_EXP_SQ8, ATTN_EXP_ROWMAX_POT = 0, 1, 2, 3, 4
-ATTN_OK, ATTN_EINVAL, ATTN_EUNSUPPORTED, ATTN_ELAUNCH = 0, -1, -2, -3
+ATTN_OK, ATTN_EINVAL, ATTN_EUNSUPPORTED, ATTN_ELAUNCH, ATTN_ENOSPACE = 0, -1, -2, -3, -4
 
 # every symbol the header declares
 EXPORTS = ("attn_fwd", "attn_fwd_ex", "attn_fwd_probe", "attn_strerror", "attn_tile_bc", "attn_decode",
-           "attn_decode_workspace_bytes", "attn_decode_split_keys", "attn_decode_probe")
+           "attn_decode_workspace_bytes", "attn_decode_split_keys", "attn_decode_probe", "attn_decode_noalloc")
 
 
 class attn_opts(ctypes.Structure):
@@ -67,6 +67,8 @@ def lib() -> ctypes.CDLL:
     dec = [P, P, P, P, P, I, I, I, I, I, I, I, I, F, I, I, I, P, ctypes.c_size_t, ctypes.POINTER(attn_opts)]
     L.attn_decode.argtypes = dec
     L.attn_decode.restype = I
+    L.attn_decode_noalloc.argtypes = dec[:17] + [ctypes.POINTER(attn_opts)]
+    L.attn_decode_noalloc.restype = I
     L.attn_decode_probe.argtypes = dec + [I, I, I, P, P, P]
     L.attn_decode_probe.restype = I
     L.attn_decode_workspace_bytes.argtypes = [I, I, I, I, I, I]
@@ -227,6 +229,23 @@ def attn_decode(q, k, v, *, causal: bool, scale: float, exp_mode: int, split_key
                            ctypes.byref(opts))
     if rc != ATTN_OK:
         raise AttnError(rc, "attn_decode")
+    return out, lse
+
+
+def attn_decode_noalloc(q, k, v, *, causal: bool, scale: float, exp_mode: int, split_keys: int,
+                        Sk: int | None = None, descale=None, stream=None, out=None, lse=None, want_lse: bool = True):
+    """attn_decode with the library's built-in workspace (see include/h15attn.h,
+    attn_decode_noalloc).  Pass out (and lse) to keep the call free of
+    allocations; calls that overlap on one GPU race on the built-in buffer."""
+    B, Hq, Hkv, Sq, Sk, cap, d, dt = _check_decode(q, k, v, Sk)
+    out, lse = _outputs(q, out, lse, want_lse)
+    opts = _opts(descale, stream)
+    rc = lib().attn_decode_noalloc(q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(),
+                                   lse.data_ptr() if lse is not None else None, B, Hq, Hkv, Sq, Sk, cap, d,
+                                   int(bool(causal)), float(scale), dt, int(exp_mode), int(split_keys),
+                                   ctypes.byref(opts))
+    if rc != ATTN_OK:
+        raise AttnError(rc, "attn_decode_noalloc")
     return out, lse
 
 

@@ -202,6 +202,7 @@ const char* attn_strerror(int code) {
     case ATTN_EINVAL: return "invalid argument";
     case ATTN_EUNSUPPORTED: return "unsupported configuration";
     case ATTN_ELAUNCH: return "kernel launch failed";
+    case ATTN_ENOSPACE: return "the decode cut needs more workspace than the built-in scratch buffer";
     default: return "unknown error code";
   }
 }
@@ -279,6 +280,25 @@ int attn_decode(const void* q, const void* k, const void* v, void* o, float* lse
                                  split_keys, opts);
   if (rc != ATTN_OK) return rc;
   const int wrc = bind_workspace(p, d, workspace, workspace_bytes);
+  if (wrc != ATTN_OK) return wrc;
+  void* st = opts ? opts->stream : nullptr;
+  return decode_launch(p, dtype, d, causal ? 1 : 0, exp_mode, st, false);
+}
+
+int attn_decode_noalloc(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq, int Hkv,
+                        int Sq, int Sk, int Sk_cap, int d, int causal, float scale, int dtype, int exp_mode,
+                        int split_keys, const attn_opts* opts) {
+  DecParams p;
+  const int rc = fill_dec_params(p, q, k, v, o, lse, B, Hq, Hkv, Sq, Sk, Sk_cap, d, scale, dtype, exp_mode,
+                                 split_keys, opts);
+  if (rc != ATTN_OK) return rc;
+  // the parts' partial results go to the built-in workspace of the current
+  // device (nothing is allocated); a cut that needs more is refused
+  const size_t need = dec_workspace_bytes((long long)B * Hq * Sq, p.nsplit, d);
+  if (need > scratch_capacity()) return ATTN_ENOSPACE;
+  void* ws = nullptr;
+  if (need > 0 && scratch_address(&ws) != 0) return ATTN_ELAUNCH;
+  const int wrc = bind_workspace(p, d, ws, need);
   if (wrc != ATTN_OK) return wrc;
   void* st = opts ? opts->stream : nullptr;
   return decode_launch(p, dtype, d, causal ? 1 : 0, exp_mode, st, false);

@@ -74,6 +74,13 @@ int launch_probe_fill(float* s, float* w, uint32_t* pbits, size_t n, void* strea
 // the parts' kernel, then (several parts) their merge
 int launch_decode(const DecParams& p, int dtype, int d, int causal, int mode, void* stream, bool probe);
 
+// The library's built-in decode workspace (h15attn.hip): its size in bytes,
+// and the address of the current device's copy (0, or nonzero when the
+// runtime cannot name the device or the address).  The address is looked up
+// once per device, on the first call with that device current.
+size_t scratch_capacity();
+int scratch_address(void** ptr);
+
 }  // namespace h15
 
 #endif  // H15ATTN_PARAMS_H

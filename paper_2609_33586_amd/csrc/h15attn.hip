@@ -28,6 +28,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "attn_params.h"
@@ -1533,9 +1534,36 @@ hipError_t launch_merge(const DecParams& dp, int dtype, int d, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Built-in workspace of attn_decode_noalloc: the parts' (m, l, O) of one
+// decode call, for callers that cannot allocate.  Each GPU the library runs
+// on holds its own copy until the process ends.  In host code the name is
+// only a stand-in for the device address: the address each device uses is
+// looked up once per device (scratch_address) and only that is passed on.
+constexpr size_t SCRATCH_BYTES = (size_t)16 << 20;
+static __device__ __align__(256) uint8_t scratch[SCRATCH_BYTES];
+
 }  // namespace
 
 namespace h15 {
+
+size_t scratch_capacity() { return SCRATCH_BYTES; }
+
+int scratch_address(void** ptr) {
+  constexpr int MAX_DEVICES = 64;
+  static std::mutex mu;
+  static void* addr[MAX_DEVICES] = {};
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES) return 1;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    // with the device current: this device's copy of the array
+    void* a = nullptr;
+    if (hipGetSymbolAddress(&a, HIP_SYMBOL(scratch)) != hipSuccess || !a) return 1;
+    addr[dev] = a;
+  }
+  *ptr = addr[dev];
+  return 0;
+}
 
 int launch_fwd(const Params& p, int dtype, int d, int causal, int mode, void* stream, bool probe) {
   hipStream_t st = (hipStream_t)stream;

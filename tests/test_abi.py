@@ -153,3 +153,17 @@ def test_decode_split_and_workspace_sizes(L):
     for args in ((1, 8, 1, 1, 100000, 128, 0), (3, 64, 8, 4, 5000, 64, 1)):
         s = pkg.attn_decode_split_keys(*args)
         assert s % 128 == 0 and s >= 0
+
+
+def test_decode_noalloc_checks(L):
+    # argument checks as attn_decode, then the built-in buffer's 16 MiB limit,
+    # all before the GPU is touched
+    E_INV = pkg.ATTN_EINVAL
+    args = [FAKE, FAKE, FAKE, FAKE, None, 4, 64, 8, 1, 16384, 16384, 128, 1, 0.1, 0, 1]
+    assert pkg.attn_decode_workspace_bytes(4, 64, 1, 16384, 128, 128) == 4 * 64 * 128 * 130 * 4 > 16 << 20
+    assert L.attn_decode_noalloc(*args, 128, None) == pkg.ATTN_ENOSPACE
+    assert L.attn_decode_noalloc(None, *args[1:], 128, None) == E_INV
+    assert L.attn_decode_noalloc(*args, 100, None) == E_INV
+    assert L.attn_decode_noalloc(*args[:9], 16385, *args[10:], 0, None) == E_INV  # Sk beyond the cache
+    assert L.attn_decode_noalloc(*args[:14], 1, 1, 128, None) == E_INV  # FP8 without descales
+    assert pkg.attn_strerror(pkg.ATTN_ENOSPACE) != pkg.attn_strerror(7)
