@@ -16,6 +16,8 @@ constexpr int BC = 128;    // keys per tile (the running max moves once per tile
 // query rows per forward workgroup: 4 waves for FP8, 8 for BF16
 constexpr int FWD_ROWS_FP8 = 4 * WROWS;
 constexpr int FWD_ROWS_BF16 = 8 * WROWS;
+// the compact layout (BF16 grids that underfill the chip): 4 waves per group
+constexpr int FWD_ROWS_COMPACT = 4 * WROWS;
 // query rows per decode workgroup
 constexpr int DEC_ROWS = WROWS;
 
@@ -40,6 +42,7 @@ struct Params {
   int tau_wave;       // 1: the anchor decision is shared by the wave's 32 rows
   int nqb;    // query blocks per head
   int remap;  // XCD-grouped workgroup order: 0 none, 1 query blocks outermost, 2 KV heads outermost
+  int compact;  // 1: the compact layout (4-wave groups, at most 80 KB of LDS; BF16 only)
   // probe target (probe launches only)
   int pb, ph, prow0, pnrows;
   float* s_out;

@@ -81,7 +81,11 @@ constexpr bool mode_lattice(int mode) { return mode != MODE_EXACT && mode != MOD
 constexpr bool mode_narrow(int mode) { return mode_lattice(mode) && mode % 2 == 0; }
 constexpr int POT_KMAX = 20;  // tail clamp of Rowmax-PoT
 
-template <int DT, int D>
+// CMP: the compact layout for grids that underfill the chip (BF16, chosen
+// per call on the host): 4 waves per group and at most 80 KB of LDS, so two
+// groups share a CU and one's prologue, barriers and epilogue overlap the
+// other's work; at d = 128 that means single-buffered K and V tiles.
+template <int DT, int D, bool CMP = false>
 struct Cfg {
   static constexpr int EB = DT == DT_BF16 ? 2 : 1;  // operand bytes
   static constexpr int RB = D * EB;                 // bytes per K/V row
@@ -89,10 +93,14 @@ struct Cfg {
   static constexpr int TILE = BC * RB;              // bytes of one K (or V) tile
   static constexpr int BUF = 2 * TILE;              // K then V
   static constexpr int CHUNKS = BC * NCH;           // 16-byte chunks per tile
-  static constexpr int NW = waves_per_group<DT>();  // waves per workgroup
-  static constexpr int BR = NW * WROWS;             // query rows per workgroup
+  static constexpr int NW = CMP ? 4 : waves_per_group<DT>();  // waves per workgroup
+  static constexpr int BR = NW * WROWS;                       // query rows per workgroup
+  // K/V tile buffers: two (the copy of tile t + 1 overlaps tile t), or one
+  // when two would not let two compact groups share a CU's 160 KB of LDS
+  static constexpr int NSTAGE = (CMP && 2 * BUF > 80 * 1024) ? 1 : 2;
   static_assert(CHUNKS % (NW * 64) == 0, "tile/staging mismatch");
-  static_assert(BR == (DT == DT_FP8 ? FWD_ROWS_FP8 : FWD_ROWS_BF16), "row block of attn_params.h");
+  static_assert(BR == (CMP ? FWD_ROWS_COMPACT : DT == DT_FP8 ? FWD_ROWS_FP8 : FWD_ROWS_BF16),
+                "row block of attn_params.h");
 };
 
 // Bank-spreading XOR swizzles of the 16-byte chunks of a row.  K rows are read
@@ -354,13 +362,14 @@ __device__ __forceinline__ float tile_sum(const f32x16 (&v)[4]) {
 // Two waves per SIMD, three for fp8 at d = 64 (163 VGPRs, 32 KB of LDS per
 // workgroup: three workgroups fit a CU, and the third wave hides more of the
 // VALU latency in that VALU-bound case).
-template <int DT, int D, bool CAUSAL, int MODE, bool PROBE>
+template <int DT, int D, bool CAUSAL, int MODE, bool PROBE, bool CMP>
 __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, (DT == DT_FP8 && D == 64) ? 3 : 2))) void
 attn_fwd_kernel(Params p) {
-  using C = Cfg<DT, D>;
+  using C = Cfg<DT, D, CMP>;
   constexpr int NW = C::NW, BR = C::BR;
-  // K and V tiles, each double-buffered
-  constexpr int NSTAGE = 2;
+  // K and V tiles, each double-buffered (or single-buffered, compact d = 128)
+  constexpr int NSTAGE = C::NSTAGE;
+  static_assert(NSTAGE == 2 || MODE != MODE_ROWMAX_POT, "the Rowmax-PoT first pass double-buffers K");
   __shared__ __attribute__((aligned(16))) uint8_t smem[NSTAGE * C::BUF];
 
   const int tid = threadIdx.x;
@@ -898,6 +907,35 @@ attn_fwd_kernel(Params p) {
   // ---- one tile per step: copy in the next tile, then QK^T, weights, PV.
   // Steps come in pairs so that each one's LDS buffers are fixed at compile
   // time and their addresses fold into the reads' immediate offsets.
+  // Single-buffered tiles (compact d = 128): K(t + 1) is copied in once every
+  // wave has read K(t), during the weights and PV of tile t, and V(t + 1)
+  // once every wave has read V(t), during QK^T of tile t + 1; each wait for a
+  // copy comes just before the barrier that makes it visible.
+  auto step_single = [&](int t) __attribute__((always_inline)) {
+    uint8_t* const kl = smem;
+    uint8_t* const vl = smem + C::TILE;
+    if (t <= last_act) {
+      __builtin_amdgcn_s_setprio(1);
+      qk(kl);
+      __builtin_amdgcn_s_setprio(0);
+      settle_scores(sacc);
+    }
+    // this wave's copy of V(t) has landed and its reads of K(t) are done
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (t + 1 < ntiles) stage(t + 1, kl, krsrc, koff_c);
+    if (t <= last_act) {
+      softmax_tile(t, vl);
+      __builtin_amdgcn_s_setprio(1);
+      pv_finish();
+      __builtin_amdgcn_s_setprio(0);
+      if constexpr (SPLIT) probe_weights(t);
+    }
+    // this wave's copy of K(t + 1) has landed and its reads of V(t) are done
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (t + 1 < ntiles) stage(t + 1, vl, vrsrc, voff_c);
+  };
   auto step = [&](int t, auto par) __attribute__((always_inline)) {
     constexpr int P = decltype(par)::value;
     uint8_t* const kl = smem + P * C::BUF;
@@ -920,13 +958,21 @@ attn_fwd_kernel(Params p) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
   };
-  stage_k(0);
-  stage_v(0);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  for (int t = 0; t < ntiles; t += 2) {
-    step(t, std::integral_constant<int, 0>{});
-    if (t + 1 < ntiles) step(t + 1, std::integral_constant<int, 1>{});
+  if constexpr (NSTAGE == 1) {
+    stage(0, smem, krsrc, koff_c);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    stage(0, smem + C::TILE, vrsrc, voff_c);
+    for (int t = 0; t < ntiles; ++t) step_single(t);
+  } else {
+    stage_k(0);
+    stage_v(0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    for (int t = 0; t < ntiles; t += 2) {
+      step(t, std::integral_constant<int, 0>{});
+      if (t + 1 < ntiles) step(t + 1, std::integral_constant<int, 1>{});
+    }
   }
 
   // ---- epilogue: O = acc / l * v_descale (bf16), LSE
@@ -969,8 +1015,16 @@ __global__ void probe_fill(float* s, float* w, uint32_t* pbits, size_t n) {
 template <int DT, int D, bool CAUSAL, int MODE, bool PROBE>
 hipError_t launch_one(const Params& p, hipStream_t st) {
   const unsigned grid = (unsigned)(p.nqb * p.B * p.Hq);
-  hipLaunchKernelGGL((attn_fwd_kernel<DT, D, CAUSAL, MODE, PROBE>), dim3(grid), dim3(Cfg<DT, D>::NW * 64), 0, st,
-                     p);
+  if constexpr (DT == DT_BF16 && MODE != MODE_ROWMAX_POT) {
+    if (p.compact) {
+      hipLaunchKernelGGL((attn_fwd_kernel<DT, D, CAUSAL, MODE, PROBE, true>), dim3(grid),
+                         dim3(Cfg<DT, D, true>::NW * 64), 0, st, p);
+      return hipGetLastError();
+    }
+  }
+  if (p.compact) return hipErrorInvalidValue;  // offered for BF16 without Rowmax-PoT only
+  hipLaunchKernelGGL((attn_fwd_kernel<DT, D, CAUSAL, MODE, PROBE, false>), dim3(grid), dim3(Cfg<DT, D>::NW * 64), 0,
+                     st, p);
   return hipGetLastError();
 }
 
