@@ -8,8 +8,11 @@
 // rows of one head per wave; two waves per SIMD, three for FP8 at d = 64):
 //   * each wave keeps its 32 query rows of Q in VGPRs as the MFMA B operand;
 //   * key tiles of 128 keys are copied HBM -> LDS with buffer loads that
-//     write LDS directly (no staging registers), double-buffered: the copy
-//     of tile t+1 is in flight while tile t is computed, one barrier per tile;
+//     write LDS directly (no staging registers), double-buffered (the copy
+//     of tile t+1 is in flight while tile t is computed, one barrier per
+//     tile) or single-buffered (K(t+1) copied while the weights and PV of
+//     tile t run, V(t+1) while QK^T of tile t+1 runs, two barriers per tile:
+//     the lattice weights at FP8 d = 128, and the compact BF16 layout);
 //   * scores are computed transposed, S^T = K Q^T, with 32x32 MFMAs (bf16
 //     32x32x16, fp8 32x32x64): each lane owns one query row and 64 of the
 //     tile's 128 keys, so the row max and row sum are in-lane reductions plus
@@ -367,8 +370,11 @@ __global__ __launch_bounds__(MAX_THREADS) __attribute__((amdgpu_waves_per_eu(2, 
 attn_fwd_kernel(Params p) {
   using C = Cfg<DT, D, CMP>;
   constexpr int NW = C::NW, BR = C::BR;
-  // K and V tiles, each double-buffered (or single-buffered, compact d = 128)
-  constexpr int NSTAGE = C::NSTAGE;
+  // K and V tiles, each double-buffered, or single-buffered: compact d = 128,
+  // and the lattice weights at FP8 d = 128 (measured at causal and
+  // non-causal 8K: H15 +1.7..2.4% single-buffered, the exact control
+  // -0.7%, so the control keeps two buffers)
+  constexpr int NSTAGE = (DT == DT_FP8 && D == 128 && mode_lattice(MODE)) ? 1 : C::NSTAGE;
   static_assert(NSTAGE == 2 || MODE != MODE_ROWMAX_POT, "the Rowmax-PoT first pass double-buffers K");
   __shared__ __attribute__((aligned(16))) uint8_t smem[NSTAGE * C::BUF];
 
@@ -1084,8 +1090,31 @@ hipError_t launch_any(const Params& p, int dtype, int d, int causal, int mode, h
 // LDS, so every wave moves the same running maximum at every tile, and the
 // waves' partial row sums and O accumulators, all relative to that maximum,
 // are added up at the end.
+//
+// Decode reads the cache once and is bound by HBM, so the copies are laid
+// out to keep as many bytes in flight as LDS allows: each wave loads only
+// its own 32 keys, K straight into its MFMA operand registers (one tile
+// ahead) and V into its own LDS slots (DEC_VSTAGES slots, so V of the next
+// DEC_VSTAGES - 1 tiles is in flight); no barrier is needed for the copies,
+// only the one per tile for the row maxima.  66 KB of LDS per group and at
+// most 256 VGPRs per lane, so two groups share a CU (measured: with four
+// times the V slots and one group per CU the per-tile chain of a lone wave
+// per SIMD left FP8 decode 50% slower; with two groups FP8 +3% and BF16
+// +11% against copies shared through double-buffered tiles).
 
 constexpr int DEC_NW = 4;  // waves per decode workgroup (one 32-key block each)
+template <int DT>
+constexpr int dec_vstages() {
+  return DT == DT_FP8 ? 4 : 2;
+}
+
+// s_waitcnt for vmcnt <= N only (gfx9 encoding: vmcnt in bits 3:0 and 15:14;
+// expcnt 6:4 and lgkmcnt 11:8 at their maxima, so not waited for)
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
 
 __device__ __forceinline__ void settle_block(f32x16& v) {
   // as settle_scores, for one block
@@ -1109,17 +1138,23 @@ __device__ __forceinline__ float block_max(const f32x16& v) {
 }
 
 template <int DT, int D, bool CAUSAL, int MODE, bool PROBE>
-__global__ __launch_bounds__(DEC_NW * 64) void attn_decode_kernel(DecParams p) {
+__global__ __launch_bounds__(DEC_NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void attn_decode_kernel(
+    DecParams p) {
   using C = Cfg<DT, D>;
   constexpr int NW = DEC_NW;
-  constexpr int NSTAGE = 2;
+  constexpr int NSV = dec_vstages<DT>();
+  constexpr int VSLOT = WROWS * C::RB;  // one wave's 32 V rows of a tile
   constexpr int NDB = D / 32;
   constexpr int NKQ = DT == DT_BF16 ? D / 16 : D / 64;
-  constexpr int CHUNKS = C::CHUNKS;
-  static_assert(CHUNKS % (NW * 64) == 0, "tile/staging mismatch");
-  static_assert(NW * NDB * 16 * 64 * 4 <= NSTAGE * C::BUF, "the O reduction reuses the tile buffers");
-  __shared__ __attribute__((aligned(16))) uint8_t smem[NSTAGE * C::BUF];
-  __shared__ __attribute__((aligned(16))) float mx_lds[32][NW];
+  constexpr int VLOADS = VSLOT / 1024;                   // 1 KB LDS copies per wave and tile
+  constexpr int KLOADS = DT == DT_BF16 ? NKQ : 2 * NKQ;  // 16-byte K loads per lane and tile
+  // loads issued after V(t) by the time tile t reads it, once every step
+  // issues its K and V copies
+  constexpr int VWAIT = (NSV - 1) * (KLOADS + VLOADS);
+  static_assert(VSLOT % 1024 == 0 && (NSV & (NSV - 1)) == 0, "V slots");
+  static_assert(NW * NDB * 16 * 64 * 4 <= NW * NSV * VSLOT, "the O reduction reuses the V slots");
+  __shared__ __attribute__((aligned(16))) uint8_t smem[NW * NSV * VSLOT];
+  __shared__ __attribute__((aligned(16))) float mx_lds[2][32][NW];
   __shared__ float l_lds[NW][64];
 
   const int tid = threadIdx.x;
@@ -1160,41 +1195,65 @@ __global__ __launch_bounds__(DEC_NW * 64) void attn_decode_kernel(DecParams p) {
     for (int kk = 0; kk < NKQ; ++kk) qf8[kk] = *(const i32x8*)(qptr + 64 * kk + 32 * g);
   }
 
-  // ---- staging of the part's tiles, as in the forward kernel; the buffer
-  // resource starts at the part's first key and ends at the cache length, so
-  // rows at or beyond Sk read as zero
+  // ---- the part's K and V rows through buffer resources that start at the
+  // part's first key and end at the cache length, so rows at or beyond Sk
+  // read as zero (those keys are masked)
   const uint8_t* kg = p.k + ((size_t)bkv * (size_t)p.Sk_cap + (size_t)j0) * C::RB;
   const uint8_t* vg = p.v + ((size_t)bkv * (size_t)p.Sk_cap + (size_t)j0) * C::RB;
   const __amdgpu_buffer_rsrc_t krsrc =
       __builtin_amdgcn_make_buffer_rsrc((void*)kg, (short)0, (Sk - j0) * C::RB, BUF_DWORD3);
   const __amdgpu_buffer_rsrc_t vrsrc =
       __builtin_amdgcn_make_buffer_rsrc((void*)vg, (short)0, (Sk - j0) * C::RB, BUF_DWORD3);
-  constexpr int WAVE_LOADS = CHUNKS / (NW * 64);
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
-  uint32_t koff_c[WAVE_LOADS], voff_c[WAVE_LOADS];
+
+  // K of this wave's 32 keys of tile t straight into the MFMA A operand
+  // (lane: key 32 wave + i32; bf16: 16 bytes at 32 kk + 16 g of the row;
+  // fp8: 32 bytes at 64 kk + 32 g)
+  using KOp = std::conditional_t<DT == DT_BF16, bf16x8, i32x8>;
+  const uint32_t krow = (uint32_t)((32 * wave + i32) * C::RB);
+  auto load_k = [&](int t, KOp (&dst)[NKQ]) __attribute__((always_inline)) {
+    const int soff = t * BC * C::RB;
 #pragma unroll
-  for (int c = 0; c < WAVE_LOADS; ++c) {
-    const int slot = (c * NW + wave) * 64 + lane;
+    for (int kk = 0; kk < NKQ; ++kk) {
+      if constexpr (DT == DT_BF16) {
+        dst[kk] = __builtin_bit_cast(
+            bf16x8, __builtin_amdgcn_raw_buffer_load_b128(krsrc, (int)(krow + 32 * kk + 16 * g), soff, 0));
+      } else {
+        const i32x4 lo = __builtin_bit_cast(
+            i32x4, __builtin_amdgcn_raw_buffer_load_b128(krsrc, (int)(krow + 64 * kk + 32 * g), soff, 0));
+        const i32x4 hi = __builtin_bit_cast(
+            i32x4, __builtin_amdgcn_raw_buffer_load_b128(krsrc, (int)(krow + 64 * kk + 32 * g + 16), soff, 0));
+        dst[kk] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+    }
+  };
+  // V of this wave's 32 keys of tile t into its LDS slot t % NSV: slot byte
+  // s holds row s / RB with the forward kernel's chunk swizzle (the swizzle
+  // depends on the row modulo 16, which the 32-row offset keeps)
+  uint32_t voff_c[VLOADS];
+#pragma unroll
+  for (int c = 0; c < VLOADS; ++c) {
+    const int slot = c * 64 + lane;
     const int r = slot / C::NCH, pch = slot % C::NCH;
-    koff_c[c] = (uint32_t)(r * C::RB + ((pch ^ k_swz<DT, D>(r)) << 4));
     voff_c[c] = (uint32_t)(r * C::RB + ((pch ^ v_swz<DT, D>(r)) << 4));
   }
-  auto stage = [&](int t, uint8_t* dst, const __amdgpu_buffer_rsrc_t& rsrc,
-                   const uint32_t (&off_c)[WAVE_LOADS]) __attribute__((always_inline)) {
-    const uint32_t soff = (uint32_t)(t * BC) * C::RB;
+  auto vslot = [&](int t) { return smem + ((t & (NSV - 1)) * NW + wave_s) * VSLOT; };
+  auto stage_v = [&](int t) __attribute__((always_inline)) {
+    const uint32_t soff = (uint32_t)((t * BC + 32 * wave_s) * C::RB);
+    uint8_t* const base = vslot(t);
 #pragma unroll
-    for (int c = 0; c < WAVE_LOADS; ++c) {
-      const uint32_t voff = off_c[c];
-      uint8_t* ldst = dst + (c * NW + wave_s) * 1024;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, LDS_PTR(void, ldst), 16, voff, soff, 0, 0);
+    for (int c = 0; c < VLOADS; ++c) {
+      const uint32_t voff = voff_c[c];
+      uint8_t* ldst = base + c * 1024;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vrsrc, LDS_PTR(void, ldst), 16, voff, soff, 0, 0);
     }
   };
 
-  // ---- V^T operand addresses (as the forward kernel's, moved to this
-  // wave's 32 keys; the swizzle repeats every 16 rows, so the move keeps it)
+  // ---- V^T operand addresses (as the forward kernel's, within this wave's
+  // slot of 32 rows)
   uint32_t vbase[NDB];
   auto set_vbase = [&](const uint8_t* vl) __attribute__((always_inline)) {
-    const uint32_t vla = (uint32_t)(size_t)LDS_PTR(const uint8_t, vl) + (uint32_t)(32 * wave * C::RB);
+    const uint32_t vla = (uint32_t)(size_t)LDS_PTR(const uint8_t, vl);
     if constexpr (DT == DT_BF16) {
       const int vrow = 4 * (G4 >> 1) + (L16 >> 2);
       const int vcolb = (16 * (G4 & 1) + 4 * (L16 & 3)) * 2;
@@ -1221,45 +1280,29 @@ __global__ __launch_bounds__(DEC_NW * 64) void attn_decode_kernel(DecParams p) {
   float l_part = 0.0f;
   const bool probe_row = PROBE && row_ok && b == p.pb && h == p.ph && iq == p.pi;
 
-  stage(0, smem, krsrc, koff_c);
-  stage(0, smem + C::TILE, vrsrc, voff_c);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  for (int t = 0; t < ntiles; ++t) {
-    uint8_t* const kl = smem + (t & 1) * C::BUF;
-    uint8_t* const vl = kl + C::TILE;
-    if (t + 1 < ntiles) {
-      stage(t + 1, smem + ((t + 1) & 1) * C::BUF, krsrc, koff_c);
-      stage(t + 1, smem + ((t + 1) & 1) * C::BUF + C::TILE, vrsrc, voff_c);
-    }
+  // K(0) and V(0 .. NSV - 2) first; step t then issues K(t + 1) and
+  // V(t + NSV - 1), in that order, before its own work
+  KOp kreg[2][NKQ];
+  load_k(0, kreg[0]);
+  for (int s = 0; s < NSV - 1; ++s)
+    if (s < ntiles) stage_v(s);
+  auto step = [&](int t, KOp (&kc)[NKQ], KOp (&kn)[NKQ]) __attribute__((always_inline)) {
+    if (t + 1 < ntiles) load_k(t + 1, kn);
+    if (t + NSV - 1 < ntiles) stage_v(t + NSV - 1);
     const int kt0 = j0 + t * BC;    // first key of the tile
     const int kw0 = kt0 + 32 * wave;  // first key of this wave's block
 
     // ---- S^T block of this wave's 32 keys
     f32x16 sv;
-    {
-      const uint8_t* rowp = kl + (32 * wave + i32) * C::RB;
-      const int kswz = k_swz<DT, D>(i32);  // == k_swz(32 wave + i32)
-      if constexpr (DT == DT_BF16) {
-        bf16x8 kop[NKQ];
+    if constexpr (DT == DT_BF16) {
 #pragma unroll
-        for (int kk = 0; kk < NKQ; ++kk) kop[kk] = *(const bf16x8*)(rowp + (((2 * kk + g) ^ kswz) << 4));
+      for (int kk = 0; kk < NKQ; ++kk)
+        sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kc[kk], qb16[kk], kk == 0 ? f32x16{0.0f} : sv, 0, 0, 0);
+    } else {
 #pragma unroll
-        for (int kk = 0; kk < NKQ; ++kk)
-          sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop[kk], qb16[kk], kk == 0 ? f32x16{0.0f} : sv, 0, 0, 0);
-      } else {
-        i32x8 kop[NKQ];
-#pragma unroll
-        for (int kk = 0; kk < NKQ; ++kk) {
-          const i32x4 lo = *(const i32x4*)(rowp + (((4 * kk + 2 * g) ^ kswz) << 4));
-          const i32x4 hi = *(const i32x4*)(rowp + (((4 * kk + 2 * g + 1) ^ kswz) << 4));
-          kop[kk] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-        }
-#pragma unroll
-        for (int kk = 0; kk < NKQ; ++kk)
-          sv = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kop[kk], qf8[kk], kk == 0 ? f32x16{0.0f} : sv, 0, 0,
-                                                               0, 0, 0, 0);
-      }
+      for (int kk = 0; kk < NKQ; ++kk)
+        sv = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kc[kk], qf8[kk], kk == 0 ? f32x16{0.0f} : sv, 0, 0, 0,
+                                                             0, 0, 0);
     }
     settle_block(sv);
 
@@ -1281,10 +1324,12 @@ __global__ __launch_bounds__(DEC_NW * 64) void attn_decode_kernel(DecParams p) {
     {
       float ma, mb;
       with_partner(block_max(sv), ma, mb);
-      if (g == 0) mx_lds[i32][wave] = __builtin_fmaxf(ma, mb);
+      if (g == 0) mx_lds[t & 1][i32][wave] = __builtin_fmaxf(ma, mb);
     }
+    // (the two copies of mx_lds alternate, so a wave that runs ahead writes
+    // the other one: every wave has read this one before the next barrier)
     __syncthreads();
-    const f32x4 mx4 = *(const f32x4*)&mx_lds[i32][0];
+    const f32x4 mx4 = *(const f32x4*)&mx_lds[t & 1][i32][0];
     const float m_new = max3(m_run, __builtin_fmaxf(mx4[0], mx4[1]), __builtin_fmaxf(mx4[2], mx4[3]));
     // a row that has seen no key yet keeps m = -inf, l = 0, O = 0
     const float alpha = m_new == -INFINITY ? 1.0f : __builtin_amdgcn_exp2f((m_run - m_new) * p.c1);
@@ -1391,8 +1436,14 @@ __global__ __launch_bounds__(DEC_NW * 64) void attn_decode_kernel(DecParams p) {
       }
     }
 
-    // ---- O^T += V^T P^T over this wave's keys
-    set_vbase(vl);
+    // ---- O^T += V^T P^T over this wave's keys, from its slot of V(t): this
+    // wave's copy of V(t) has landed once at most VWAIT later loads are
+    // outstanding (when every step so far issued its copies), or none is.
+    // (The probe's stores also count as outstanding memory operations, so
+    // the probe waits for all.)
+    if (!PROBE && t >= NSV - 1 && t + NSV - 1 < ntiles) wait_vmcnt<VWAIT>();
+    else wait_vmcnt<0>();
+    set_vbase(vslot(t));
     if constexpr (DT == DT_BF16) {
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
@@ -1424,9 +1475,16 @@ __global__ __launch_bounds__(DEC_NW * 64) void attn_decode_kernel(DecParams p) {
         oacc[db] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(vop, pf, oacc[db], 0, 0, 0, 0, 0, 0);
       }
     }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+  };
+  // tiles in pairs, so that each step's K registers are fixed at compile time
+  for (int t = 0; t < ntiles; t += 2) {
+    step(t, kreg[0], kreg[1]);
+    if (t + 1 < ntiles) step(t + 1, kreg[1], kreg[0]);
   }
+  // every copy has landed and every wave is done with its V slots before the
+  // slots are reused for the reduction
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
 
   // ---- the four waves' partial sums: O^T blocks and row sums through LDS
   {
