@@ -4,7 +4,7 @@
 // (App. B.2), or Rowmax-PoT (App. A.6), behind the C ABI declared in
 // h15attn.h.
 //
-// Kernel structure (one workgroup = 4 wave64s for FP8, 8 for BF16; 32 query
+// Kernel structure (one workgroup = 4 wave64s for FP8, 8 or 4 for BF16; 32 query
 // rows of one head per wave; two waves per SIMD, three for FP8 at d = 64):
 //   * each wave keeps its 32 query rows of Q in VGPRs as the MFMA B operand;
 //   * key tiles of 128 keys are copied HBM -> LDS with buffer loads that
@@ -57,9 +57,10 @@ typedef short i16x2 __attribute__((ext_vector_type(2)));
 
 enum { DT_BF16 = 0, DT_FP8 = 1 };
 
-// Waves per workgroup: 4 for FP8 (two workgroups share a CU, so one's
-// barrier and prologue stalls overlap the other's work), 8 for BF16 (whose
-// double-buffered tiles leave LDS for only one workgroup per CU).
+// Waves per workgroup in the default layout: 4 for FP8 (two workgroups
+// share a CU, so one's barrier and prologue stalls overlap the other's
+// work), 8 for BF16 (whose double-buffered tiles at d = 128 leave LDS for
+// only one workgroup per CU; the compact layout, Cfg below, has 4).
 template <int DT>
 constexpr int waves_per_group() {
   return DT == DT_FP8 ? 4 : 8;
