@@ -219,10 +219,13 @@ int attn_decode_split_keys(int B, int Hq, int Hkv, int Sq, int Sk, int d, int dt
  * before the merge reads them).  The first call on a device looks up that
  * device's buffer with the device current.
  *
- * Errors: those of attn_decode (without the workspace ones), and
- * ATTN_ENOSPACE when attn_decode_workspace_bytes() of the shape and cut
- * exceeds 16 MiB (16777216 bytes; choose a coarser cut, or use attn_decode);
- * nothing is launched then. */
+ * The buffer used is the current device's, so a stream passed in opts must
+ * belong to the current device.
+ *
+ * Errors: those of attn_decode (without the workspace ones); ATTN_ENOSPACE
+ * when attn_decode_workspace_bytes() of the shape and cut exceeds 16 MiB
+ * (16777216 bytes; choose a coarser cut, or use attn_decode); ATTN_EINVAL
+ * when the stream belongs to another device; nothing is launched then. */
 int attn_decode_noalloc(const void* q, const void* k, const void* v, void* o, float* lse, int B, int Hq, int Hkv,
                         int Sq, int Sk, int Sk_cap, int d, int causal, float scale, int dtype, int exp_mode,
                         int split_keys, const attn_opts* opts);

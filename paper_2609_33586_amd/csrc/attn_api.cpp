@@ -317,11 +317,15 @@ int attn_decode_noalloc(const void* q, const void* k, const void* v, void* o, fl
   // device (nothing is allocated); a cut that needs more is refused
   const size_t need = dec_workspace_bytes((long long)B * Hq * Sq, p.nsplit, d);
   if (need > scratch_capacity()) return ATTN_ENOSPACE;
+  void* st = opts ? opts->stream : nullptr;
   void* ws = nullptr;
-  if (need > 0 && scratch_address(&ws) != 0) return ATTN_ELAUNCH;
+  if (need > 0) {
+    const int src = scratch_address(st, &ws);
+    if (src == 2) return ATTN_EINVAL;
+    if (src != 0) return ATTN_ELAUNCH;
+  }
   const int wrc = bind_workspace(p, d, ws, need);
   if (wrc != ATTN_OK) return wrc;
-  void* st = opts ? opts->stream : nullptr;
   return decode_launch(p, dtype, d, causal ? 1 : 0, exp_mode, st, false);
 }
 

@@ -78,11 +78,13 @@ int launch_probe_fill(float* s, float* w, uint32_t* pbits, size_t n, void* strea
 int launch_decode(const DecParams& p, int dtype, int d, int causal, int mode, void* stream, bool probe);
 
 // The library's built-in decode workspace (h15attn.hip): its size in bytes,
-// and the address of the current device's copy (0, or nonzero when the
-// runtime cannot name the device or the address).  The address is looked up
-// once per device, on the first call with that device current.
+// and the address of the current device's copy for work on stream (NULL:
+// the default stream).  Returns 0; 1 when the runtime cannot name the
+// device, the stream's device or the address; 2 when the stream belongs to
+// another device than the current one.  The address is looked up once per
+// device, on the first call with that device current.
 size_t scratch_capacity();
-int scratch_address(void** ptr);
+int scratch_address(void* stream, void** ptr);
 
 }  // namespace h15
 

@@ -1661,12 +1661,19 @@ namespace h15 {
 
 size_t scratch_capacity() { return SCRATCH_BYTES; }
 
-int scratch_address(void** ptr) {
+int scratch_address(void* stream, void** ptr) {
   constexpr int MAX_DEVICES = 64;
   static std::mutex mu;
   static void* addr[MAX_DEVICES] = {};
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES) return 1;
+  if (stream) {
+    // the kernels run on the stream's device: its buffer is the one to use,
+    // and it is looked up with the current device, so the two must agree
+    hipDevice_t sdev = -1;
+    if (hipStreamGetDevice((hipStream_t)stream, &sdev) != hipSuccess) return 1;
+    if (sdev != dev) return 2;
+  }
   std::lock_guard<std::mutex> lock(mu);
   if (!addr[dev]) {
     // with the device current: this device's copy of the array

@@ -16,7 +16,7 @@ int launch_probe_fill(float*, float*, uint32_t*, size_t, void*) { return ++g_lau
 int launch_decode(const DecParams&, int, int, int, int, void*, bool) { return ++g_launches, 1; }
 // the built-in decode workspace: the library's stated size, no address
 size_t scratch_capacity() { return (size_t)16 << 20; }
-int scratch_address(void**) { return ++g_launches, 1; }
+int scratch_address(void*, void**) { return ++g_launches, 1; }
 
 }  // namespace h15
 

@@ -39,6 +39,18 @@ def run_pair(case, seed):
     torch.cuda.synchronize()
     assert torch.equal(o.view(torch.int16), o_ref.view(torch.int16))
     assert torch.equal(lse, l_ref)
+    # the same on a side stream of the current device
+    st = torch.cuda.Stream()
+    o2 = torch.full_like(o_ref, float("nan"))
+    lse2 = torch.full_like(l_ref, float("nan"))
+    torch.cuda.synchronize()
+    with torch.cuda.stream(st):
+        pkg.attn_decode_noalloc(q, k, v, causal=causal, scale=sc, exp_mode=mode, split_keys=split,
+                                descale=inp.descale, stream=st, out=o2, lse=lse2)
+    st.synchronize()
+    torch.cuda.synchronize()
+    assert torch.equal(o2.view(torch.int16), o_ref.view(torch.int16))
+    assert torch.equal(lse2, l_ref)
 
 
 @pytest.mark.parametrize("first,second", [(0, 1), (2, 3)])
