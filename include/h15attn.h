@@ -201,7 +201,7 @@ int attn_decode(const void* q, const void* k, const void* v, void* o, float* lse
 size_t attn_decode_workspace_bytes(int B, int Hq, int Sq, int Sk, int d, int split_keys);
 
 /* A cut (split_keys) for attn_decode that gives about two workgroups per
- * compute unit with at least four key tiles per part, or 0 (one part) when
+ * compute unit with at least eight key tiles per part, or 0 (one part) when
  * the shape fills the GPU without cutting.  A function of its arguments
  * only; 0 for invalid sizes. */
 int attn_decode_split_keys(int B, int Hq, int Hkv, int Sq, int Sk, int d, int dtype);

@@ -144,8 +144,8 @@ def test_decode_split_and_workspace_sizes(L):
     assert pkg.attn_decode_workspace_bytes(1, 4, 1, 1000, 128, 0) == 0       # one part
     assert pkg.attn_decode_workspace_bytes(1, 4, 1, 1000, 128, 1024) == 0    # one part
     assert pkg.attn_decode_workspace_bytes(2, 8, 3, 1000, 64, 128) == 2 * 8 * 3 * 8 * 66 * 4
-    # the proposed cut: whole tiles, about 512 workgroups, at least four tiles each
-    assert pkg.attn_decode_split_keys(1, 32, 8, 1, 32768, 128, 0) == 512     # 8 groups x 64 parts
+    # the proposed cut: whole tiles, about 512 workgroups, at least eight tiles each
+    assert pkg.attn_decode_split_keys(1, 32, 8, 1, 32768, 128, 0) == 1024    # 8 groups x 32 parts of 8 tiles
     assert pkg.attn_decode_split_keys(16, 32, 8, 1, 8192, 128, 1) == 2048    # 128 groups x 4 parts
     assert pkg.attn_decode_split_keys(64, 32, 8, 1, 4096, 128, 0) == 0       # 512 groups: no cut
     assert pkg.attn_decode_split_keys(1, 8, 8, 1, 600, 128, 0) == 0          # under eight tiles
