@@ -337,7 +337,7 @@ def main():
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the attention forward is timed on a single MI355X "
               f"(--gpus {args.gpus} is not supported; head/batch sharding across GPUs needs no "
-              f"communication and is described in DESIGN.md).", file=sys.stderr)
+              f"communication: each GPU would run this kernel on its share of the heads).", file=sys.stderr)
         sys.exit(2)
 
     import torch
