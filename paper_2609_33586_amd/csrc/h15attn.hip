@@ -987,14 +987,21 @@ attn_fwd_kernel(Params p) {
   float la, lb;
   with_partner(l_part, la, lb);
   const float l = la + lb;
-  if (qrow >= S) return;
   const float inv = p.vd / l;
-  uint16_t* orow = p.o + (q_head + qrow) * (size_t)D;
+  // O leaves through LDS, which is free once every wave has passed the last
+  // barrier: the lanes write their four-column pieces into the wave's own
+  // 32 x D block (16-byte chunks XOR-swizzled by row, so that neither side
+  // conflicts on the banks) and read back 16 contiguous bytes of a row, so
+  // that each global store covers whole rows instead of 8 bytes in each of
+  // 32 rows
+  constexpr int ORB = D * 2, ONC = ORB / 16;  // bytes and 16-byte chunks per O row
+  static_assert(NW * WROWS * ORB <= NSTAGE * C::BUF, "O staging fits the tile buffers");
+  uint8_t* const ost = smem + wave * (WROWS * ORB);
+  auto oswz = [](int row) { return D == 128 ? (row & 15) : ((row >> 1) & 7); };
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
     for (int jq = 0; jq < 4; ++jq) {
-      const int col = 32 * db + 8 * jq + 4 * g;
       const __bf16 a0 = (__bf16)(oacc[db][4 * jq + 0] * inv);
       const __bf16 a1 = (__bf16)(oacc[db][4 * jq + 1] * inv);
       const __bf16 a2 = (__bf16)(oacc[db][4 * jq + 2] * inv);
@@ -1003,9 +1010,31 @@ attn_fwd_kernel(Params p) {
                            ((uint32_t)__builtin_bit_cast(uint16_t, a1) << 16);
       const uint32_t w23 = (uint32_t)__builtin_bit_cast(uint16_t, a2) |
                            ((uint32_t)__builtin_bit_cast(uint16_t, a3) << 16);
-      *(u32x2*)(orow + col) = u32x2{w01, w23};
+      // columns 32 db + 8 jq + 4 g .. +3: chunk 4 db + jq, half g
+      *(u32x2*)(ost + i32 * ORB + (((4 * db + jq) ^ oswz(i32)) << 4) + 8 * g) = u32x2{w01, w23};
     }
-  if (p.lse && g == 0)
+  // the wave reads what its other lanes wrote (LDS keeps a wave's order)
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  constexpr int RPI = 64 / ONC;  // rows per store
+  const int rsub = lane / ONC, csub = lane % ONC;
+  uint8_t* const obase = (uint8_t*)p.o + (q_head + qw0) * (size_t)ORB + csub * 16;
+  u32x4 orows[WROWS / RPI];
+#pragma unroll
+  for (int k = 0; k < WROWS / RPI; ++k) {
+    const int r = RPI * k + rsub;
+    orows[k] = *(const u32x4*)(ost + r * ORB + ((csub ^ oswz(r)) << 4));
+  }
+  if (qw0 + WROWS <= S) {
+#pragma unroll
+    for (int k = 0; k < WROWS / RPI; ++k) *(u32x4*)(obase + (size_t)(RPI * k + rsub) * ORB) = orows[k];
+  } else {
+#pragma unroll
+    for (int k = 0; k < WROWS / RPI; ++k)
+      if (qw0 + RPI * k + rsub < S) *(u32x4*)(obase + (size_t)(RPI * k + rsub) * ORB) = orows[k];
+  }
+  if (p.lse && g == 0 && qrow < S)
     p.lse[q_head + qrow] = 0.69314718055994531f * (m_run * p.c1 + log2f(l) - off);
 }
 
