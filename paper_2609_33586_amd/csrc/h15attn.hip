@@ -403,18 +403,11 @@ attn_fwd_kernel(Params p) {
   const uint8_t* vg = p.v + kv_head * C::RB;
   const size_t q_head = (size_t)(b * p.Hq + h) * (size_t)S;
 
-  // ---- Q block in registers (MFMA B operand: lane holds row i32, k-half g)
+  // ---- Q block in registers (MFMA B operand: lane holds row i32, k-half g);
+  // loaded through LDS below (stage_q, read_q)
   constexpr int NKQ = DT == DT_BF16 ? D / 16 : D / 64;
-  const uint8_t* qptr = p.q + (q_head + min(qrow, S - 1)) * C::RB;
   bf16x8 qb16[DT == DT_BF16 ? NKQ : 1];
   i32x8 qf8[DT == DT_FP8 ? NKQ : 1];
-  if constexpr (DT == DT_BF16) {
-#pragma unroll
-    for (int kk = 0; kk < NKQ; ++kk) qb16[kk] = *(const bf16x8*)(qptr + (16 * kk + 8 * g) * 2);
-  } else {
-#pragma unroll
-    for (int kk = 0; kk < NKQ; ++kk) qf8[kk] = *(const i32x8*)(qptr + 64 * kk + 32 * g);
-  }
 
   // ---- staging: every wave copies WAVE_LOADS x 1 KB of a K or V tile
   // straight into LDS.  LDS slot s (16 bytes) of a tile holds row s / NCH,
@@ -459,6 +452,46 @@ attn_fwd_kernel(Params p) {
   };
   auto stage_k = [&](int t) { stage(t, kbuf(t), krsrc, koff_c); };
   auto stage_v = [&](int t) { stage(t, vbuf(t), vrsrc, voff_c); };
+
+  // ---- Q through LDS: each wave copies its own 32 rows with the same
+  // direct loads (16 contiguous bytes per lane, so each load covers whole
+  // rows; rows at or beyond S read as zero), into a region the first K/V
+  // copies do not touch (the V buffer when single-buffered, else the second
+  // buffer), chunks swizzled as K's so that the operand reads, one chunk of
+  // 32 rows per instruction like K's, spread over the banks.  Every wave
+  // reads its operands before any wave copies into that region again (a
+  // barrier after read_q).
+  constexpr int QBYTES = WROWS * C::RB;
+  constexpr int QREGION = NSTAGE == 1 ? C::TILE : C::BUF;
+  static_assert(QBYTES % 1024 == 0 && QREGION + NW * QBYTES <= NSTAGE * C::BUF, "Q staging layout");
+  const __amdgpu_buffer_rsrc_t qrsrc =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(p.q + q_head * C::RB), (short)0, S * C::RB, BUF_DWORD3);
+  uint8_t* const qreg = smem + QREGION + wave_s * QBYTES;
+  auto stage_q = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int c = 0; c < QBYTES / 1024; ++c) {
+      const int slot = c * 64 + lane;
+      const int row = slot / C::NCH, pch = slot % C::NCH;
+      const uint32_t voff = (uint32_t)((qw0 + row) * C::RB + ((pch ^ k_swz<DT, D>(row)) << 4));
+      uint8_t* ldst = qreg + c * 1024;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(qrsrc, LDS_PTR(void, ldst), 16, voff, 0, 0, 0);
+    }
+  };
+  auto read_q = [&]() __attribute__((always_inline)) {
+    const uint8_t* const qrow_l = qreg + i32 * C::RB;
+    const int qswz = k_swz<DT, D>(i32);
+    if constexpr (DT == DT_BF16) {
+#pragma unroll
+      for (int kk = 0; kk < NKQ; ++kk) qb16[kk] = *(const bf16x8*)(qrow_l + (((2 * kk + g) ^ qswz) << 4));
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < NKQ; ++kk) {
+        const i32x4 lo = *(const i32x4*)(qrow_l + (((4 * kk + 2 * g) ^ qswz) << 4));
+        const i32x4 hi = *(const i32x4*)(qrow_l + (((4 * kk + 2 * g + 1) ^ qswz) << 4));
+        qf8[kk] = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+    }
+  };
 
   // ---- running state (this lane's query row; lanes i and i^32 agree on m)
   constexpr int NDB = D / 32;  // 32-column blocks of O^T
@@ -890,8 +923,11 @@ attn_fwd_kernel(Params p) {
   if constexpr (MODE == MODE_ROWMAX_POT) {
     // ---- Rowmax-PoT anchors every weight at the whole-row maximum: a first
     // pass over the key tiles computes it (QK^T and the masked row max only)
+    stage_q();
     stage_k(0);
     __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    read_q();
     __syncthreads();
     for (int t = 0; t < ntiles; ++t) {
       if (t + 1 < ntiles) stage_k(t + 1);
@@ -966,16 +1002,24 @@ attn_fwd_kernel(Params p) {
     __syncthreads();
   };
   if constexpr (NSTAGE == 1) {
+    stage_q();
     stage(0, smem, krsrc, koff_c);
     __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    read_q();
     __syncthreads();
     stage(0, smem + C::TILE, vrsrc, voff_c);
     for (int t = 0; t < ntiles; ++t) step_single(t);
   } else {
+    if constexpr (MODE != MODE_ROWMAX_POT) stage_q();
     stage_k(0);
     stage_v(0);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+    if constexpr (MODE != MODE_ROWMAX_POT) {
+      read_q();
+      __syncthreads();
+    }
     for (int t = 0; t < ntiles; t += 2) {
       step(t, std::integral_constant<int, 0>{});
       if (t + 1 < ntiles) step(t + 1, std::integral_constant<int, 1>{});
