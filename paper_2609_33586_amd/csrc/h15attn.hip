@@ -6,7 +6,8 @@
 //
 // Kernel structure (one workgroup = 4 wave64s for FP8, 8 or 4 for BF16; 32 query
 // rows of one head per wave; two waves per SIMD, three for FP8 at d = 64):
-//   * each wave keeps its 32 query rows of Q in VGPRs as the MFMA B operand;
+//   * each wave keeps its 32 query rows of Q in VGPRs as the MFMA B operand,
+//     brought in through LDS with whole-row loads;
 //   * key tiles of 128 keys are copied HBM -> LDS with buffer loads that
 //     write LDS directly (no staging registers), double-buffered (the copy
 //     of tile t+1 is in flight while tile t is computed, one barrier per
@@ -26,7 +27,8 @@
 //     and ds_read_b64_tr_b8 (fp8), in the matching key order;
 //   * at fp8 the PV MFMAs over the tile's first 64 keys go first, and the
 //     weights of the other 64 are finished between them (split P), so that
-//     a wave's VALU work overlaps its own matrix-core work.
+//     a wave's VALU work overlaps its own matrix-core work;
+//   * O leaves through LDS, so that each store covers whole rows.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
