@@ -111,12 +111,22 @@ def _check(q, k, v):
 
 
 def _outputs(q, out, lse, want_lse):
+    """O [B,Hq,S,d] bf16 and LSE [B,Hq,S] fp32 (None unless wanted or given):
+    the caller's tensors after checks, else new ones.  The library writes
+    through the data pointers, so a given tensor must be contiguous, of the
+    right shape and type, and on q's device."""
     import torch
     B, Hq, S, d = q.shape
     if out is None:
         out = torch.empty((B, Hq, S, d), dtype=torch.bfloat16, device=q.device)
+    elif (tuple(out.shape) != (B, Hq, S, d) or out.dtype != torch.bfloat16 or not out.is_contiguous()
+          or out.device != q.device):
+        raise ValueError(f"out must be a contiguous bfloat16 tensor {(B, Hq, S, d)} on {q.device}")
     if lse is None and want_lse:
         lse = torch.empty((B, Hq, S), dtype=torch.float32, device=q.device)
+    elif lse is not None and (tuple(lse.shape) != (B, Hq, S) or lse.dtype != torch.float32
+                              or not lse.is_contiguous() or lse.device != q.device):
+        raise ValueError(f"lse must be a contiguous float32 tensor {(B, Hq, S)} on {q.device}")
     return out, lse
 
 
@@ -206,6 +216,8 @@ def _workspace(q, B, Hq, Sq, Sk, d, split_keys, workspace):
     need = attn_decode_workspace_bytes(B, Hq, Sq, Sk, d, split_keys)
     if workspace is None:
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device) if need else None
+    elif not workspace.is_contiguous() or workspace.device != q.device:
+        raise ValueError(f"workspace must be a contiguous tensor on {q.device}")
     ptr = workspace.data_ptr() if workspace is not None else None
     nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     return workspace, ptr, nbytes

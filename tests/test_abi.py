@@ -167,3 +167,30 @@ def test_decode_noalloc_checks(L):
     assert L.attn_decode_noalloc(*args[:9], 16385, *args[10:], 0, None) == E_INV  # Sk beyond the cache
     assert L.attn_decode_noalloc(*args[:14], 1, 1, 128, None) == E_INV  # FP8 without descales
     assert pkg.attn_strerror(pkg.ATTN_ENOSPACE) != pkg.attn_strerror(7)
+
+
+def test_binding_checks_given_outputs():
+    # the library writes through the data pointers it is given, so the
+    # binding refuses output tensors it could not write as [B,Hq,S,d] bf16 /
+    # [B,Hq,S] fp32 row-major (checked on host tensors: no GPU needed)
+    import torch
+    q = torch.zeros((2, 4, 40, 64), dtype=torch.bfloat16)
+    good_o = torch.empty((2, 4, 40, 64), dtype=torch.bfloat16)
+    good_l = torch.empty((2, 4, 40), dtype=torch.float32)
+    o, l = pkg._outputs(q, good_o, good_l, True)
+    assert o is good_o and l is good_l
+    assert pkg._outputs(q, good_o, None, False)[1] is None
+    bad_o = [torch.empty((2, 4, 40, 128), dtype=torch.bfloat16),             # shape
+             torch.empty((2, 4, 40, 64), dtype=torch.float32),               # type
+             torch.empty((2, 4, 64, 40), dtype=torch.bfloat16).transpose(2, 3)]  # not contiguous
+    for t in bad_o:
+        with pytest.raises(ValueError):
+            pkg._outputs(q, t, good_l, True)
+    bad_l = [torch.empty((2, 4, 41), dtype=torch.float32), torch.empty((2, 4, 40), dtype=torch.bfloat16),
+             torch.empty((2, 40, 4), dtype=torch.float32).transpose(1, 2)]
+    for t in bad_l:
+        with pytest.raises(ValueError):
+            pkg._outputs(q, good_o, t, True)
+    ws = torch.empty((64, 2), dtype=torch.uint8).t()
+    with pytest.raises(ValueError):
+        pkg._workspace(q, 2, 4, 40, 1000, 64, 128, ws)

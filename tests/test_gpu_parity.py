@@ -305,6 +305,37 @@ def test_xcd_grouped_orders_write_every_row(dt):
                      causal=causal, sc=sc, rows=rows)
 
 
+GUARD_SHAPES = [(BF16, 1, 4, 2, 333, 64), (BF16, 1, 4, 2, 333, 128), (FP8, 1, 4, 2, 333, 128),
+                (FP8, 2, 3, 3, 129, 64), (BF16, 1, 64, 8, 2500, 128)]  # the last: BF16's 8-wave layout
+
+
+@pytest.mark.parametrize("dt,B,Hq,Hkv,S,d", GUARD_SHAPES)
+def test_writes_stay_inside_outputs(dt, B, Hq, Hkv, S, d):
+    # O and LSE as views into larger NaN-filled buffers: every element of the
+    # views is written, nothing before or after them is, and the result equals
+    # that of a call with outputs of their own (the O rows leave through LDS;
+    # the last query block is ragged)
+    inp = synth.make_inputs(B, Hq, Hkv, S, d, dt, sharp=True, seed=700 + S + d)
+    sc = scale_of(d)
+    q, k, v = dev_tensors(inp)
+    G = 4096
+    n_o, n_l = B * Hq * S * d, B * Hq * S
+    for causal in (False, True):
+        for mode in (EXACT, H15):
+            say(f"guard dtype={dt} shape={(B, Hq, Hkv, S, d)} causal={causal} mode={mode}")
+            ob = torch.full((G + n_o + G,), float("nan"), dtype=torch.bfloat16, device="cuda:0")
+            lb = torch.full((G + n_l + G,), float("nan"), dtype=torch.float32, device="cuda:0")
+            o = ob[G:G + n_o].view(B, Hq, S, d)
+            lse = lb[G:G + n_l].view(B, Hq, S)
+            pkg.attn_fwd_ex(q, k, v, causal=causal, scale=sc, exp_mode=mode, descale=inp.descale, out=o, lse=lse)
+            o2, l2 = pkg.attn_fwd_ex(q, k, v, causal=causal, scale=sc, exp_mode=mode, descale=inp.descale)
+            torch.cuda.synchronize()
+            assert torch.isnan(ob[:G].float()).all() and torch.isnan(ob[G + n_o:].float()).all()
+            assert torch.isnan(lb[:G]).all() and torch.isnan(lb[G + n_l:]).all()
+            assert not torch.isnan(o.float()).any() and not torch.isnan(lse).any()
+            assert torch.equal(o.view(torch.int16), o2.view(torch.int16)) and torch.equal(lse, l2)
+
+
 EDGE = [(1, 1, 1, 1, 64), (1, 1, 1, 2, 128), (1, 2, 1, 31, 128), (2, 3, 3, 129, 64), (1, 8, 1, 255, 128),
         (3, 4, 2, 257, 128), (1, 16, 2, 1000, 128)]
 
