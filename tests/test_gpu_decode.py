@@ -183,6 +183,35 @@ def test_deterministic_and_every_row_written():
         assert torch.equal(o1.view(torch.int16), o2.view(torch.int16)) and torch.equal(l1, l2)
 
 
+@pytest.mark.parametrize("dt,d", [(BF16, 64), (FP8, 128)])
+def test_writes_stay_inside_outputs(dt, d):
+    # O, LSE and the workspace as views into larger NaN-filled buffers: the
+    # guard regions on both sides stay untouched, with one part and with
+    # several (the parts' partial results, then the merge)
+    B, Hq, Hkv, Sq, Sk = 2, 8, 2, 3, 1000
+    inp = synth.make_decode_inputs(B, Hq, Hkv, Sq, Sk, d, dt, sharp=True, seed=1750 + d)
+    q, k, v = dev_tensors(inp)
+    sc = scale_of(d)
+    G = 4096
+    n_o, n_l = B * Hq * Sq * d, B * Hq * Sq
+    for split in (0, 256):
+        say(f"decode guard dtype={dt} d={d} split={split}")
+        ob = torch.full((G + n_o + G,), float("nan"), dtype=torch.bfloat16, device="cuda:0")
+        lb = torch.full((G + n_l + G,), float("nan"), dtype=torch.float32, device="cuda:0")
+        need = pkg.attn_decode_workspace_bytes(B, Hq, Sq, Sk, d, split)
+        wb = torch.full((G + max(need, 16) + G,), 0x5A, dtype=torch.uint8, device="cuda:0")
+        o, lse = ob[G:G + n_o].view(B, Hq, Sq, d), lb[G:G + n_l].view(B, Hq, Sq)
+        pkg.attn_decode(q, k, v, causal=True, scale=sc, exp_mode=H15, split_keys=split, descale=inp.descale,
+                        out=o, lse=lse, workspace=wb[G:G + max(need, 16)])
+        o2, l2 = pkg.attn_decode(q, k, v, causal=True, scale=sc, exp_mode=H15, split_keys=split,
+                                 descale=inp.descale)
+        torch.cuda.synchronize()
+        assert torch.isnan(ob[:G].float()).all() and torch.isnan(ob[G + n_o:].float()).all()
+        assert torch.isnan(lb[:G]).all() and torch.isnan(lb[G + n_l:]).all()
+        assert (wb[:G] == 0x5A).all() and (wb[G + max(need, 16):] == 0x5A).all()
+        assert torch.equal(o.view(torch.int16), o2.view(torch.int16)) and torch.equal(lse, l2)
+
+
 DECODE_FULL = [("bf16", BF16), ("fp8", FP8)]
 
 
