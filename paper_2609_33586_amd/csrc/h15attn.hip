@@ -474,7 +474,9 @@ attn_fwd_kernel(Params p) {
     for (int c = 0; c < QBYTES / 1024; ++c) {
       const int slot = c * 64 + lane;
       const int row = slot / C::NCH, pch = slot % C::NCH;
-      const uint32_t voff = (uint32_t)((qw0 + row) * C::RB + ((pch ^ k_swz<DT, D>(row)) << 4));
+      // (unsigned: rows past S may take the offset past 2^31, where the
+      // range check still reads zero)
+      const uint32_t voff = (uint32_t)(qw0 + row) * (uint32_t)C::RB + (uint32_t)((pch ^ k_swz<DT, D>(row)) << 4);
       uint8_t* ldst = qreg + c * 1024;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(qrsrc, LDS_PTR(void, ldst), 16, voff, 0, 0, 0);
     }
@@ -1036,10 +1038,10 @@ attn_fwd_kernel(Params p) {
   const float inv = p.vd / l;
   // O leaves through LDS, which is free once every wave has passed the last
   // barrier: the lanes write their four-column pieces into the wave's own
-  // 32 x D block (16-byte chunks XOR-swizzled by row, so that neither side
-  // conflicts on the banks) and read back 16 contiguous bytes of a row, so
-  // that each global store covers whole rows instead of 8 bytes in each of
-  // 32 rows
+  // 32 x D block (16-byte chunks XOR-swizzled by row: the reads are free of
+  // bank conflicts, the writes of rows r and r + 16 share banks) and read
+  // back 16 contiguous bytes of a row, so that each global store covers
+  // whole rows instead of 8 bytes in each of 32 rows
   constexpr int ORB = D * 2, ONC = ORB / 16;  // bytes and 16-byte chunks per O row
   static_assert(NW * WROWS * ORB <= NSTAGE * C::BUF, "O staging fits the tile buffers");
   uint8_t* const ost = smem + wave * (WROWS * ORB);
