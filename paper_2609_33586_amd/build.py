@@ -11,6 +11,7 @@ Flags that matter:
 from __future__ import annotations
 
 import os
+import shutil
 import subprocess
 import sys
 from pathlib import Path
@@ -49,34 +50,42 @@ UNITS = [
 
 
 def build(extra: list[str] | None = None, verbose: bool = False) -> Path:
-    tmp = LIB_PATH.with_name(LIB_PATH.name + ".tmp")
-    compile_flags = [f for f in HIPCC_FLAGS if f != "-shared"]
-    objs, procs = [], []
-    for name, src, flags in UNITS:
-        obj = LIB_PATH.with_name(f".{LIB_PATH.stem}.{name}.o")
-        cmd = [hipcc(), *compile_flags, *flags, *(extra or []), f"-I{INCLUDE}", f"-I{src.parent}", "-c", str(src),
-               "-o", str(obj)]
-        procs.append((name, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)))
-        objs.append(obj)
-    failed = []
-    for name, proc in procs:
-        out, err = proc.communicate()
-        if proc.returncode != 0:
-            sys.stderr.write(out + err)
-            failed.append(name)
-        elif verbose:
-            sys.stderr.write(err)
-    if failed:
-        raise RuntimeError(f"hipcc failed building {', '.join(failed)} of {LIB_PATH.name}")
-    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *map(str, objs), "-o", str(tmp)]
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    for obj in objs:
-        obj.unlink(missing_ok=True)
-    if res.returncode != 0:
-        sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError(f"hipcc failed ({res.returncode}) linking {LIB_PATH.name}")
-    check_kernel_stubs(tmp)
-    tmp.replace(LIB_PATH)
+    import tempfile
+    objdir = Path(tempfile.mkdtemp(prefix="h15attn-build-"))
+    try:
+        compile_flags = [f for f in HIPCC_FLAGS if f != "-shared"]
+        objs, procs = [], []
+        for name, src, flags in UNITS:
+            obj = objdir / f"{name}.o"
+            cmd = [hipcc(), *compile_flags, *flags, *(extra or []), f"-I{INCLUDE}", f"-I{src.parent}", "-c",
+                   str(src), "-o", str(obj)]
+            procs.append((name, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)))
+            objs.append(obj)
+        failed = []
+        for name, proc in procs:
+            out, err = proc.communicate()
+            if proc.returncode != 0:
+                sys.stderr.write(out + err)
+                failed.append(name)
+            elif verbose:
+                sys.stderr.write(err)
+        if failed:
+            raise RuntimeError(f"hipcc failed building {', '.join(failed)} of {LIB_PATH.name}")
+        linked = objdir / LIB_PATH.name
+        cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *map(str, objs), "-o", str(linked)]
+        res = subprocess.run(cmd, capture_output=True, text=True)
+        if res.returncode != 0:
+            sys.stderr.write(res.stdout + res.stderr)
+            raise RuntimeError(f"hipcc failed ({res.returncode}) linking {LIB_PATH.name}")
+        check_kernel_stubs(linked)
+        # the temporary folder may sit on another file system: copy next to
+        # the target, then rename over it
+        staged = LIB_PATH.with_name(LIB_PATH.name + ".tmp")
+        shutil.copyfile(linked, staged)
+        staged.chmod(0o755)
+        staged.replace(LIB_PATH)
+    finally:
+        shutil.rmtree(objdir, ignore_errors=True)
     return LIB_PATH
 
 
