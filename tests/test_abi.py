@@ -194,3 +194,19 @@ def test_binding_checks_given_outputs():
     ws = torch.empty((64, 2), dtype=torch.uint8).t()
     with pytest.raises(ValueError):
         pkg._workspace(q, 2, 4, 40, 1000, 64, 128, ws)
+
+
+def test_library_links_both_kernel_units(L):
+    # the kernel file is compiled twice (the FP8 lattice-weight forward at
+    # d = 128 on its own): the library must hold that unit's launcher and
+    # exactly one launch stub per forward kernel instantiation
+    import subprocess
+    out = subprocess.run(["nm", "-C", str(pkg.LIB_PATH)], capture_output=True, text=True, check=True).stdout
+    assert re.search(r"\bT h15::launch_fwd_fp8_lattice128\(", out)
+    stubs = re.findall(r"__device_stub__attn_fwd_kernel<(\d), (\d+), (true|false), (\d), (true|false), (true|false)>",
+                       out)
+    assert len(stubs) == len(set(stubs))
+    lattice128 = {s for s in stubs if s[0] == "1" and s[1] == "128" and s[3] != "0"}
+    assert len(lattice128) == 2 * 6 * 2  # causal x the six lattice modes x probe
+    # BF16: d x causal x probe x (5 default + 4 compact); FP8: d x causal x probe x 7 modes
+    assert len(stubs) == 2 * 2 * 2 * 9 + 2 * 2 * 2 * 7
